@@ -1,0 +1,235 @@
+/*
+ * readme.h -- C ABI of libreadme, the MI355X (gfx950) hot path of a
+ * pre-gated mixture-of-experts layer (Read-ME, arXiv 2410.19123).
+ *
+ * The paper replaces per-layer routers with one router evaluated once per
+ * token ahead of all layers (Sec. 2.3, Eq. 2): a token's expert index is
+ * known before layer 1 and is the same at every layer.  With top-1 routing a
+ * layer's output for token t is the FFN of its one expert,
+ *     y_t = F_{e_t}(x_t),
+ * and tokens can be batched by expert across requests (Sec. 4.2, Alg. 1).
+ * Each expert is a slice of a dense FFN's intermediate neurons (Sec. 3), here
+ * the SwiGLU FFN of the Llama family (Table 1):
+ *     F_e(x) = W_down^e ( silu(W_gate^e x) * (W_up^e x) ).
+ *
+ * The calls, in path order:
+ *     readme_route            one top-1 expert id per token
+ *     readme_group_by_expert  histogram, exclusive scan, stable permutation,
+ *                             row gather into expert-contiguous order
+ *     readme_moe_ffn          every expert's SwiGLU FFN on its token block
+ *                             (= readme_moe_gate_up then readme_moe_down)
+ *     readme_ungroup          rows back to token order
+ *     readme_moe_ffn_stack    L stacked pre-norm residual layers in grouped
+ *                             order (routing and grouping done once)
+ *
+ * Conventions for every call:
+ *   - Arrays are DEVICE pointers owned by the caller, row-major, contiguous.
+ *     The library keeps no state and owns no memory between calls.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Calls only enqueue work on it: they never synchronise, allocate or
+ *     free, and they read no device data on the host, so a caller may
+ *     capture them in a graph.
+ *   - Element type `dt` is README_F32 (fp32 throughout) or README_BF16 (bf16
+ *     inputs, weights and outputs, fp32 accumulation).
+ *   - The return value is README_OK, or an error found on the host before
+ *     anything is enqueued (README_ERR_ARG / _UNSUPPORTED / _WORKSPACE), or
+ *     README_ERR_HIP if a launch failed.  On an error nothing was enqueued
+ *     unless the code is README_ERR_HIP.
+ *   - Outputs must not alias inputs.  Arrays the kernels stream (token rows,
+ *     weights, packed experts, workspaces) must be 16-byte aligned; a
+ *     misaligned pointer is README_ERR_ARG.
+ *   - T = 0 is allowed and enqueues nothing (readme_group_by_expert still
+ *     writes zero counts and offsets).
+ */
+#ifndef README_H
+#define README_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t readme_status;
+#define README_OK 0
+#define README_ERR_ARG 1          /* NULL pointer, negative size, bad value */
+#define README_ERR_UNSUPPORTED 2  /* a size or type outside the supported set */
+#define README_ERR_WORKSPACE 3    /* a buffer smaller than its stated size */
+#define README_ERR_HIP 4          /* the HIP runtime refused a launch */
+
+typedef int32_t readme_dtype;
+#define README_F32 0
+#define README_BF16 1
+
+#define README_MAX_EXPERTS 256
+
+/* Human-readable name of a status code (static storage). */
+const char *readme_status_string(readme_status s);
+
+/* Version of this ABI (bumped on any signature or layout change). */
+int32_t readme_abi_version(void);
+
+/*
+ * readme_route -- the pre-gating router's top-1 choice (Eq. 2 with K = 1).
+ *
+ *   logit[t][e] = sum_k x[t][k] * w_router[e][k] + bias[e]
+ *   expert_ids[t] = the e of largest logit; ties go to the lowest index and
+ *                   a NaN logit never wins (strict '>' scan from e = 0).
+ *
+ * The paper's router is a one-block transformer over the token prefix; this
+ * call is its final gate, a linear map d -> E applied to given features.
+ * The argmax decides an integer, so the logits are summed in one fixed fp32
+ * order, identical on every run and on any GPU: 16-byte chunks of x and
+ * w_router (8 bf16 or 4 fp32 values) are dealt round-robin to 64 partial
+ * sums (chunk c to partial c mod 64), each partial fuses multiply-adds in
+ * ascending k starting from +0, the 64 partials are folded pairwise
+ * (p[l] += p[l + off] for off = 32, 16, 8, 4, 2, 1), then the bias is added.
+ *
+ *   x          [T][d]  dt          token features
+ *   w_router   [E][d]  dt          router weight
+ *   bias       [E]     fp32        or NULL (no bias)
+ *   expert_ids [T]     int32 out
+ *   logits     [T][E]  fp32 out    or NULL
+ * Requires 1 <= E <= README_MAX_EXPERTS, d > 0, d a multiple of 8 (bf16) or
+ * 4 (fp32).
+ */
+readme_status readme_route(readme_dtype dt, int64_t T, int64_t d, int32_t E,
+                           const void *x, const void *w_router,
+                           const float *bias, int32_t *expert_ids,
+                           float *logits, void *stream);
+
+/*
+ * readme_group_by_expert -- batch tokens by expert (the per-expert queues of
+ * Alg. 1; the same grouping serves every layer because a token's expert does
+ * not change between layers).
+ *
+ *   counts[e]    number of tokens with id e
+ *   offsets[e]   exclusive scan of counts; offsets[E] = routed tokens
+ *   perm[j]      token at grouped row j: expert blocks in order, tokens of
+ *                one expert in ascending token order (a stable sort)
+ *   inv_perm[t]  grouped row of token t
+ *   x_grouped[j] = x[perm[j]]   (if x and x_grouped are both non-NULL)
+ * An id outside [0, E) routes the token nowhere: it is left out of counts,
+ * inv_perm[t] = -1, and rows j >= offsets[E] have perm[j] = -1 and a zero
+ * x_grouped row.  Callers detect such ids by offsets[E] < T.
+ *
+ *   expert_ids [T] int32, counts [E] int32 out, offsets [E+1] int32 out,
+ *   perm [T] int32 out, inv_perm [T] int32 out,
+ *   x [T][d] dt, x_grouped [T][d] dt out (both NULL: no gather).
+ * Requires 1 <= E <= README_MAX_EXPERTS, T < 2^31; with a gather, d > 0 and
+ * d * element size a multiple of 16 bytes.
+ */
+readme_status readme_group_by_expert(int64_t T, int32_t E,
+                                     const int32_t *expert_ids,
+                                     int32_t *counts, int32_t *offsets,
+                                     int32_t *perm, int32_t *inv_perm,
+                                     readme_dtype dt, int64_t d,
+                                     const void *x, void *x_grouped,
+                                     void *stream);
+
+/*
+ * Expert weights are taken in their natural layout and repacked once into
+ * the layout the FFN kernels stream (gate and up rows interleaved so that
+ * one tile produces matching g and u columns, the intermediate width padded
+ * with zero neurons to a multiple of 64; zero neurons add exact zeros since
+ * silu(0) * 0 = 0).  The packed buffer is opaque; its size is
+ * readme_packed_experts_bytes().
+ *
+ *   w_gate [E][I][d], w_up [E][I][d], w_down [E][d][I]   dt
+ *   packed  >= readme_packed_experts_bytes(dt, E, d, I) bytes, out
+ * Requires 1 <= E <= README_MAX_EXPERTS, I >= 1, d > 0 a multiple of 64.
+ */
+size_t readme_packed_experts_bytes(readme_dtype dt, int32_t E, int64_t d,
+                                   int64_t I);
+readme_status readme_pack_experts(readme_dtype dt, int32_t E, int64_t d,
+                                  int64_t I, const void *w_gate,
+                                  const void *w_up, const void *w_down,
+                                  void *packed, size_t packed_bytes,
+                                  void *stream);
+
+/* Padded intermediate width of the packed layout: I rounded up to 64. */
+int64_t readme_padded_intermediate(int64_t I);
+
+/*
+ * readme_moe_ffn -- each expert's SwiGLU FFN on its token block (Eq. 2 with
+ * a fixed top-1 expert; the output is the expert's, unweighted).
+ *
+ *   for every e, every j in [offsets[e], offsets[e+1]):
+ *     h[j]         = silu(W_gate^e x_grouped[j]) * (W_up^e x_grouped[j])
+ *     y_grouped[j] = W_down^e h[j]
+ * Rows j >= offsets[E] of y_grouped are not written.
+ *
+ *   x_grouped [T][d] dt, offsets [E+1] int32 (device; non-decreasing, within
+ *   [0, T]), packed (from readme_pack_experts with the same dt, E, d, I),
+ *   y_grouped [T][d] dt out,
+ *   workspace >= readme_moe_ffn_workspace_bytes(dt, T, I) bytes (holds h).
+ * Requires d > 0 a multiple of 64, 1 <= E <= README_MAX_EXPERTS, I >= 1.
+ * Offsets are read on the device only; a block range past T is clipped.
+ */
+size_t readme_moe_ffn_workspace_bytes(readme_dtype dt, int64_t T, int64_t I);
+readme_status readme_moe_ffn(readme_dtype dt, int64_t T, int64_t d,
+                             int32_t E, int64_t I, const void *x_grouped,
+                             const int32_t *offsets, const void *packed,
+                             void *y_grouped, void *workspace,
+                             size_t workspace_bytes, void *stream);
+
+/*
+ * The two halves of readme_moe_ffn, for callers that time or overlap them:
+ *   readme_moe_gate_up: h[j][i] = silu(g) * u for i < I, and 0 for the pad
+ *     columns I <= i < readme_padded_intermediate(I);
+ *     h [T][readme_padded_intermediate(I)] dt out.
+ *   readme_moe_down:    y_grouped[j] = W_down^e h[j].
+ */
+readme_status readme_moe_gate_up(readme_dtype dt, int64_t T, int64_t d,
+                                 int32_t E, int64_t I, const void *x_grouped,
+                                 const int32_t *offsets, const void *packed,
+                                 void *h, void *stream);
+readme_status readme_moe_down(readme_dtype dt, int64_t T, int64_t d,
+                              int32_t E, int64_t I, const void *h,
+                              const int32_t *offsets, const void *packed,
+                              void *y_grouped, void *stream);
+
+/*
+ * readme_ungroup -- rows back to token order: y[t] = y_grouped[inv_perm[t]],
+ * and a zero row where inv_perm[t] < 0 (an unrouted token).
+ *   y_grouped [T][d] dt, inv_perm [T] int32, y [T][d] dt out.
+ * Requires d * element size a multiple of 16 bytes.
+ */
+readme_status readme_ungroup(readme_dtype dt, int64_t T, int64_t d,
+                             const void *y_grouped, const int32_t *inv_perm,
+                             void *y, void *stream);
+
+/*
+ * readme_moe_ffn_stack -- L stacked MoE layers of one decode or prefill step,
+ * run in grouped order.  The router runs once and a token's expert is the
+ * same at every layer (Sec. 2.3 and Sec. 4.2), so grouping is done once and
+ * the residual stream stays grouped across layers:
+ *   for l = 0 .. L-1:
+ *     r_j   = 1 / sqrt(mean_k x[j][k]^2 + rms_eps)        (fp32)
+ *     xn_j  = bf16(x[j] * r_j)
+ *     x[j] += F^l_{e(j)}(xn_j)                            (fp32 residual)
+ * (pre-norm residual layers without a norm gain, which would fold into
+ * W_gate and W_up).  bf16 weights only.
+ *
+ *   packed_per_layer  HOST array of L device pointers, each packed with
+ *                     readme_pack_experts(README_BF16, E, d, I, ...)
+ *   offsets [E+1] int32 (device), x_resid_grouped [T][d] fp32 in/out,
+ *   workspace >= readme_moe_ffn_stack_workspace_bytes(T, d, I) bytes.
+ * Requires d > 0 a multiple of 64, 1 <= E <= README_MAX_EXPERTS, I >= 1,
+ * L >= 0, rms_eps >= 0.  Rows j >= offsets[E] are left unchanged.
+ */
+size_t readme_moe_ffn_stack_workspace_bytes(int64_t T, int64_t d, int64_t I);
+readme_status readme_moe_ffn_stack(int64_t T, int64_t d, int32_t E,
+                                   int64_t I, int32_t L,
+                                   const void *const *packed_per_layer,
+                                   const int32_t *offsets,
+                                   float *x_resid_grouped, float rms_eps,
+                                   void *workspace, size_t workspace_bytes,
+                                   void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* README_H */

@@ -1,0 +1,240 @@
+"""ctypes binding of libreadme (include/readme.h), one function per C entry.
+
+Argument marshalling only: tensors become device pointers, the current torch
+stream becomes the stream argument, and a nonzero status raises.  Outputs the
+caller does not pass are allocated with torch (device memory plumbing); all
+arithmetic runs in the library's HIP kernels.  There is no fallback: if the
+library is missing or no GPU is present, calls fail loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libreadme.so")
+
+README_F32, README_BF16 = 0, 1
+README_MAX_EXPERTS = 256
+
+_STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported size or type",
+           3: "buffer smaller than required", 4: "HIP launch failed"}
+
+# (name, restype, argtypes) of every exported symbol of readme.h.
+_P, _I64, _I32, _SZ, _F = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                           ctypes.c_size_t, ctypes.c_float)
+SIGNATURES = {
+    "readme_status_string": (ctypes.c_char_p, [_I32]),
+    "readme_abi_version": (_I32, []),
+    "readme_route": (_I32, [_I32, _I64, _I64, _I32, _P, _P, _P, _P, _P, _P]),
+    "readme_group_by_expert": (_I32, [_I64, _I32, _P, _P, _P, _P, _P, _I32, _I64,
+                                      _P, _P, _P]),
+    "readme_packed_experts_bytes": (_SZ, [_I32, _I32, _I64, _I64]),
+    "readme_pack_experts": (_I32, [_I32, _I32, _I64, _I64, _P, _P, _P, _P, _SZ, _P]),
+    "readme_padded_intermediate": (_I64, [_I64]),
+    "readme_moe_ffn_workspace_bytes": (_SZ, [_I32, _I64, _I64]),
+    "readme_moe_ffn": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _SZ, _P]),
+    "readme_moe_gate_up": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P]),
+    "readme_moe_down": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P]),
+    "readme_ungroup": (_I32, [_I32, _I64, _I64, _P, _P, _P, _P]),
+    "readme_moe_ffn_stack_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
+    "readme_moe_ffn_stack": (_I32, [_I64, _I64, _I32, _I64, _I32, _P, _P, _P, _F, _P,
+                                    _SZ, _P]),
+}
+
+_lib = None
+
+
+class ReadmeError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn}: status {status} ({_STATUS.get(status, 'unknown')})")
+        self.status = status
+
+
+def load() -> ctypes.CDLL:
+    """Load libreadme.so (built in-tree by paper_2410_19123_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run "
+                              "`python -m paper_2410_19123_amd.build` first")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def _call(name: str, *args) -> None:
+    st = getattr(load(), name)(*args)
+    if st != 0:
+        raise ReadmeError(name, st)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return README_F32
+    if t.dtype == torch.bfloat16:
+        return README_BF16
+    raise ValueError(f"unsupported dtype {t.dtype}")
+
+
+def _dev(*ts):
+    for t in ts:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError("libreadme takes device tensors")
+        if not t.is_contiguous():
+            raise ValueError("libreadme takes contiguous tensors")
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def readme_route(x, w_router, bias=None, expert_ids=None, logits=None):
+    """Top-1 expert id per token; returns (expert_ids, logits or None)."""
+    T, d = x.shape
+    E = w_router.shape[0]
+    if expert_ids is None:
+        expert_ids = torch.empty(T, dtype=torch.int32, device=x.device)
+    _dev(x, w_router, bias, expert_ids, logits)
+    if w_router.dtype != x.dtype or w_router.shape[1] != d:
+        raise ValueError("w_router must be [E][d] of x's dtype")
+    if bias is not None and (bias.dtype != torch.float32 or bias.numel() != E):
+        raise ValueError("bias must be fp32 [E]")
+    _call("readme_route", _dt(x), T, d, E, _p(x), _p(w_router), _p(bias), _p(expert_ids),
+          _p(logits), _stream(x.device))
+    return expert_ids, logits
+
+
+def readme_group_by_expert(expert_ids, E, x=None, counts=None, offsets=None, perm=None,
+                           inv_perm=None, x_grouped=None):
+    """Group tokens by expert; returns (counts, offsets, perm, inv_perm, x_grouped)."""
+    T = expert_ids.shape[0]
+    dev = expert_ids.device
+    counts = counts if counts is not None else torch.empty(E, dtype=torch.int32, device=dev)
+    offsets = offsets if offsets is not None else torch.empty(E + 1, dtype=torch.int32, device=dev)
+    perm = perm if perm is not None else torch.empty(T, dtype=torch.int32, device=dev)
+    inv_perm = inv_perm if inv_perm is not None else torch.empty(T, dtype=torch.int32, device=dev)
+    if x is not None and x_grouped is None:
+        x_grouped = torch.empty_like(x)
+    _dev(expert_ids, counts, offsets, perm, inv_perm, x, x_grouped)
+    dt = _dt(x) if x is not None else README_BF16
+    d = x.shape[1] if x is not None else 0
+    _call("readme_group_by_expert", T, E, _p(expert_ids), _p(counts), _p(offsets), _p(perm),
+          _p(inv_perm), dt, d, _p(x), _p(x_grouped), _stream(dev))
+    return counts, offsets, perm, inv_perm, x_grouped
+
+
+def readme_padded_intermediate(I: int) -> int:
+    return int(load().readme_padded_intermediate(I))
+
+
+def readme_packed_experts_bytes(dtype, E, d, I) -> int:
+    return int(load().readme_packed_experts_bytes(_dt(torch.empty(0, dtype=dtype)), E, d, I))
+
+
+def readme_pack_experts(w_gate, w_up, w_down, packed=None):
+    """Repack [E][I][d], [E][I][d], [E][d][I] expert weights; returns packed bytes."""
+    E, I, d = w_gate.shape
+    dt = _dt(w_gate)
+    nbytes = readme_packed_experts_bytes(w_gate.dtype, E, d, I)
+    if packed is None:
+        packed = torch.empty(nbytes, dtype=torch.uint8, device=w_gate.device)
+    _dev(w_gate, w_up, w_down, packed)
+    if w_up.shape != w_gate.shape or w_down.shape != (E, d, I):
+        raise ValueError("expert weight shapes disagree")
+    if w_up.dtype != w_gate.dtype or w_down.dtype != w_gate.dtype:
+        raise ValueError("expert weight dtypes disagree")
+    _call("readme_pack_experts", dt, E, d, I, _p(w_gate), _p(w_up), _p(w_down), _p(packed),
+          packed.numel() * packed.element_size(), _stream(w_gate.device))
+    return packed
+
+
+def readme_moe_ffn_workspace_bytes(dtype, T, I) -> int:
+    return int(load().readme_moe_ffn_workspace_bytes(_dt(torch.empty(0, dtype=dtype)), T, I))
+
+
+def readme_moe_ffn(x_grouped, offsets, packed, E, I, y_grouped=None, workspace=None):
+    """Every expert's SwiGLU FFN on its grouped token block; returns y_grouped."""
+    T, d = x_grouped.shape
+    if y_grouped is None:
+        y_grouped = torch.empty_like(x_grouped)
+    ws = readme_moe_ffn_workspace_bytes(x_grouped.dtype, T, I)
+    if workspace is None:
+        workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=x_grouped.device)
+    _dev(x_grouped, offsets, packed, y_grouped, workspace)
+    _call("readme_moe_ffn", _dt(x_grouped), T, d, E, I, _p(x_grouped), _p(offsets), _p(packed),
+          _p(y_grouped), _p(workspace), workspace.numel() * workspace.element_size(),
+          _stream(x_grouped.device))
+    return y_grouped
+
+
+def readme_moe_gate_up(x_grouped, offsets, packed, E, I, h=None):
+    """h = silu(W_gate x) * (W_up x) per grouped row; returns h [T][I padded]."""
+    T, d = x_grouped.shape
+    if h is None:
+        h = torch.empty(T, readme_padded_intermediate(I), dtype=x_grouped.dtype,
+                        device=x_grouped.device)
+    _dev(x_grouped, offsets, packed, h)
+    _call("readme_moe_gate_up", _dt(x_grouped), T, d, E, I, _p(x_grouped), _p(offsets),
+          _p(packed), _p(h), _stream(x_grouped.device))
+    return h
+
+
+def readme_moe_down(h, offsets, packed, E, I, d, y_grouped=None):
+    """y = W_down h per grouped row; returns y_grouped [T][d]."""
+    T = h.shape[0]
+    if y_grouped is None:
+        y_grouped = torch.empty(T, d, dtype=h.dtype, device=h.device)
+    _dev(h, offsets, packed, y_grouped)
+    _call("readme_moe_down", _dt(h), T, d, E, I, _p(h), _p(offsets), _p(packed),
+          _p(y_grouped), _stream(h.device))
+    return y_grouped
+
+
+def readme_ungroup(y_grouped, inv_perm, y=None):
+    """Rows back to token order; returns y."""
+    T, d = y_grouped.shape
+    if y is None:
+        y = torch.empty_like(y_grouped)
+    _dev(y_grouped, inv_perm, y)
+    _call("readme_ungroup", _dt(y_grouped), T, d, _p(y_grouped), _p(inv_perm), _p(y),
+          _stream(y_grouped.device))
+    return y
+
+
+def readme_moe_ffn_stack_workspace_bytes(T, d, I) -> int:
+    return int(load().readme_moe_ffn_stack_workspace_bytes(T, d, I))
+
+
+def readme_moe_ffn_stack(x_resid_grouped, offsets, packed_layers, E, I, rms_eps=1e-5,
+                         workspace=None):
+    """Run len(packed_layers) pre-norm residual MoE layers in place on x (fp32)."""
+    T, d = x_resid_grouped.shape
+    if x_resid_grouped.dtype != torch.float32:
+        raise ValueError("the residual stream is fp32")
+    L = len(packed_layers)
+    ws = readme_moe_ffn_stack_workspace_bytes(T, d, I)
+    if workspace is None:
+        workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=x_resid_grouped.device)
+    _dev(x_resid_grouped, offsets, workspace, *packed_layers)
+    ptrs = (ctypes.c_void_p * max(L, 1))(*[p.data_ptr() for p in packed_layers])
+    _call("readme_moe_ffn_stack", T, d, E, I, L, ctypes.cast(ptrs, ctypes.c_void_p),
+          _p(offsets), _p(x_resid_grouped), float(rms_eps), _p(workspace),
+          workspace.numel() * workspace.element_size(), _stream(x_resid_grouped.device))
+    return x_resid_grouped
+
+
+def readme_status_string(status: int) -> str:
+    return load().readme_status_string(status).decode()

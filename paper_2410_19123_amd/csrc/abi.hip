@@ -1,0 +1,226 @@
+// C ABI of libreadme: argument checks on the host, then asynchronous
+// launches on the caller's stream.  Nothing here reads device memory,
+// synchronises, allocates or frees.
+#include <limits.h>
+
+#include "common.hpp"
+#include "internal.hpp"
+
+using namespace readme;
+
+namespace {
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+inline bool dtype_ok(readme_dtype dt) { return dt == README_F32 || dt == README_BF16; }
+inline bool experts_ok(int32_t E) { return E >= 1 && E <= README_MAX_EXPERTS; }
+inline readme_status hip_status(hipError_t e) { return e == hipSuccess ? README_OK : README_ERR_HIP; }
+// The kernels move 16-byte vectors: every array they stream must be 16-byte
+// aligned (row lengths are checked separately).
+inline bool a16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+readme_status check_ffn_shape(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I) {
+    if (!dtype_ok(dt) || T < 0 || d <= 0 || I < 1) return README_ERR_ARG;
+    if (!experts_ok(E) || d % 64 != 0 || T > INT32_MAX) return README_ERR_UNSUPPORTED;
+    return README_OK;
+}
+
+GemmArgs gate_up_args(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I,
+                      const void* xg, const int32_t* offsets, const void* packed, void* h) {
+    const int64_t Ip = padded_I(I);
+    GemmArgs g{};
+    g.A = xg;
+    g.lda = d;
+    g.B = packed;
+    g.ldb = d;
+    g.b_expert_stride = 2 * Ip * d;
+    g.N = 2 * Ip;
+    g.K = d;
+    g.offsets = offsets;
+    g.E = E;
+    g.T = T;
+    g.C = h;
+    g.ldc = Ip;
+    (void)dt;
+    return g;
+}
+
+GemmArgs down_args(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I, const void* h,
+                   const int32_t* offsets, const void* packed, void* y) {
+    const int64_t Ip = padded_I(I);
+    GemmArgs g{};
+    g.A = h;
+    g.lda = Ip;
+    g.B = reinterpret_cast<const char*>(packed) + packed_gate_up_bytes(dt, E, d, I);
+    g.ldb = Ip;
+    g.b_expert_stride = d * Ip;
+    g.N = d;
+    g.K = Ip;
+    g.offsets = offsets;
+    g.E = E;
+    g.T = T;
+    g.C = y;
+    g.ldc = d;
+    return g;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* readme_status_string(readme_status s) {
+    switch (s) {
+        case README_OK: return "ok";
+        case README_ERR_ARG: return "invalid argument";
+        case README_ERR_UNSUPPORTED: return "unsupported size or type";
+        case README_ERR_WORKSPACE: return "buffer smaller than required";
+        case README_ERR_HIP: return "HIP launch failed";
+        default: return "unknown status";
+    }
+}
+
+int32_t readme_abi_version(void) { return 1; }
+
+int64_t readme_padded_intermediate(int64_t I) { return I < 1 ? 0 : padded_I(I); }
+
+readme_status readme_route(readme_dtype dt, int64_t T, int64_t d, int32_t E, const void* x,
+                           const void* w_router, const float* bias, int32_t* expert_ids,
+                           float* logits, void* stream) {
+    if (!dtype_ok(dt) || T < 0 || d <= 0) return README_ERR_ARG;
+    if (!experts_ok(E) || T > INT32_MAX) return README_ERR_UNSUPPORTED;
+    if (d % (dt == README_BF16 ? 8 : 4) != 0) return README_ERR_UNSUPPORTED;
+    if (T == 0) return README_OK;
+    if (!x || !w_router || !expert_ids) return README_ERR_ARG;
+    if (!a16(x) || !a16(w_router)) return README_ERR_ARG;
+    return hip_status(launch_route(dt, T, d, E, x, w_router, bias, expert_ids, logits,
+                                   as_stream(stream)));
+}
+
+readme_status readme_group_by_expert(int64_t T, int32_t E, const int32_t* expert_ids,
+                                     int32_t* counts, int32_t* offsets, int32_t* perm,
+                                     int32_t* inv_perm, readme_dtype dt, int64_t d,
+                                     const void* x, void* x_grouped, void* stream) {
+    if (T < 0) return README_ERR_ARG;
+    if (!experts_ok(E) || T > INT32_MAX) return README_ERR_UNSUPPORTED;
+    if (!counts || !offsets) return README_ERR_ARG;
+    if (T > 0 && (!expert_ids || !perm || !inv_perm)) return README_ERR_ARG;
+    const bool gather = x || x_grouped;
+    if (gather) {
+        if (!x || !x_grouped || !dtype_ok(dt) || d <= 0) return README_ERR_ARG;
+        if ((d * (int64_t)dtype_size(dt)) % 16 != 0) return README_ERR_UNSUPPORTED;
+        if (!a16(x) || !a16(x_grouped)) return README_ERR_ARG;
+    }
+    hipStream_t s = as_stream(stream);
+    hipError_t err = launch_group(T, E, expert_ids, counts, offsets, perm, inv_perm, s);
+    if (err == hipSuccess && gather && T > 0)
+        err = launch_move_rows(T, d * (int64_t)dtype_size(dt), x, perm, T, x_grouped, s);
+    return hip_status(err);
+}
+
+size_t readme_packed_experts_bytes(readme_dtype dt, int32_t E, int64_t d, int64_t I) {
+    if (!dtype_ok(dt) || !experts_ok(E) || d <= 0 || I < 1) return 0;
+    return packed_bytes(dt, E, d, I);
+}
+
+readme_status readme_pack_experts(readme_dtype dt, int32_t E, int64_t d, int64_t I,
+                                  const void* w_gate, const void* w_up, const void* w_down,
+                                  void* packed, size_t packed_bytes_given, void* stream) {
+    readme_status st = check_ffn_shape(dt, 0, d, E, I);
+    if (st != README_OK) return st;
+    if (!w_gate || !w_up || !w_down || !packed) return README_ERR_ARG;
+    if (!a16(packed)) return README_ERR_ARG;
+    if (packed_bytes_given < packed_bytes(dt, E, d, I)) return README_ERR_WORKSPACE;
+    return hip_status(launch_pack(dt, E, d, I, w_gate, w_up, w_down, packed, as_stream(stream)));
+}
+
+size_t readme_moe_ffn_workspace_bytes(readme_dtype dt, int64_t T, int64_t I) {
+    if (!dtype_ok(dt) || T < 0 || I < 1) return 0;
+    return (size_t)T * padded_I(I) * dtype_size(dt);
+}
+
+readme_status readme_moe_gate_up(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I,
+                                 const void* x_grouped, const int32_t* offsets,
+                                 const void* packed, void* h, void* stream) {
+    readme_status st = check_ffn_shape(dt, T, d, E, I);
+    if (st != README_OK) return st;
+    if (T == 0) return README_OK;
+    if (!x_grouped || !offsets || !packed || !h) return README_ERR_ARG;
+    if (!a16(x_grouped) || !a16(packed)) return README_ERR_ARG;
+    GemmArgs g = gate_up_args(dt, T, d, E, I, x_grouped, offsets, packed, h);
+    return hip_status(
+        launch_grouped_gemm(dt == README_F32, EPI_GATE_UP_SILU, g, as_stream(stream)));
+}
+
+readme_status readme_moe_down(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I,
+                              const void* h, const int32_t* offsets, const void* packed,
+                              void* y_grouped, void* stream) {
+    readme_status st = check_ffn_shape(dt, T, d, E, I);
+    if (st != README_OK) return st;
+    if (T == 0) return README_OK;
+    if (!h || !offsets || !packed || !y_grouped) return README_ERR_ARG;
+    if (!a16(h) || !a16(packed)) return README_ERR_ARG;
+    GemmArgs g = down_args(dt, T, d, E, I, h, offsets, packed, y_grouped);
+    return hip_status(launch_grouped_gemm(dt == README_F32, EPI_STORE, g, as_stream(stream)));
+}
+
+readme_status readme_moe_ffn(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I,
+                             const void* x_grouped, const int32_t* offsets, const void* packed,
+                             void* y_grouped, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+    readme_status st = check_ffn_shape(dt, T, d, E, I);
+    if (st != README_OK) return st;
+    if (T == 0) return README_OK;
+    if (!x_grouped || !offsets || !packed || !y_grouped || !workspace) return README_ERR_ARG;
+    if (workspace_bytes < readme_moe_ffn_workspace_bytes(dt, T, I)) return README_ERR_WORKSPACE;
+    st = readme_moe_gate_up(dt, T, d, E, I, x_grouped, offsets, packed, workspace, stream);
+    if (st != README_OK) return st;
+    return readme_moe_down(dt, T, d, E, I, workspace, offsets, packed, y_grouped, stream);
+}
+
+readme_status readme_ungroup(readme_dtype dt, int64_t T, int64_t d, const void* y_grouped,
+                             const int32_t* inv_perm, void* y, void* stream) {
+    if (!dtype_ok(dt) || T < 0 || d <= 0) return README_ERR_ARG;
+    if (T > INT32_MAX || (d * (int64_t)dtype_size(dt)) % 16 != 0) return README_ERR_UNSUPPORTED;
+    if (T == 0) return README_OK;
+    if (!y_grouped || !inv_perm || !y) return README_ERR_ARG;
+    if (!a16(y_grouped) || !a16(y)) return README_ERR_ARG;
+    return hip_status(launch_move_rows(T, d * (int64_t)dtype_size(dt), y_grouped, inv_perm, T, y,
+                                       as_stream(stream)));
+}
+
+size_t readme_moe_ffn_stack_workspace_bytes(int64_t T, int64_t d, int64_t I) {
+    if (T < 0 || d <= 0 || I < 1) return 0;
+    return (size_t)T * d * 2 + (size_t)T * padded_I(I) * 2;
+}
+
+readme_status readme_moe_ffn_stack(int64_t T, int64_t d, int32_t E, int64_t I, int32_t L,
+                                   const void* const* packed_per_layer, const int32_t* offsets,
+                                   float* x_resid_grouped, float rms_eps, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+    readme_status st = check_ffn_shape(README_BF16, T, d, E, I);
+    if (st != README_OK) return st;
+    if (L < 0 || !(rms_eps >= 0.0f)) return README_ERR_ARG;
+    if (T == 0 || L == 0) return README_OK;
+    if (!packed_per_layer || !offsets || !x_resid_grouped || !workspace) return README_ERR_ARG;
+    if (!a16(x_resid_grouped) || !a16(workspace)) return README_ERR_ARG;
+    for (int32_t l = 0; l < L; ++l)
+        if (!packed_per_layer[l] || !a16(packed_per_layer[l])) return README_ERR_ARG;
+    if (workspace_bytes < readme_moe_ffn_stack_workspace_bytes(T, d, I))
+        return README_ERR_WORKSPACE;
+    hipStream_t s = as_stream(stream);
+    uint16_t* xn = reinterpret_cast<uint16_t*>(workspace);
+    uint16_t* h = xn + T * d;
+    for (int32_t l = 0; l < L; ++l) {
+        hipError_t err = launch_rms_to_bf16(T, d, x_resid_grouped, offsets, E, rms_eps, xn, s);
+        if (err != hipSuccess) return README_ERR_HIP;
+        GemmArgs gu = gate_up_args(README_BF16, T, d, E, I, xn, offsets, packed_per_layer[l], h);
+        err = launch_grouped_gemm(false, EPI_GATE_UP_SILU, gu, s);
+        if (err != hipSuccess) return README_ERR_HIP;
+        GemmArgs dn = down_args(README_BF16, T, d, E, I, h, offsets, packed_per_layer[l],
+                                x_resid_grouped);
+        err = launch_grouped_gemm(false, EPI_RESID_ADD, dn, s);
+        if (err != hipSuccess) return README_ERR_HIP;
+    }
+    return README_OK;
+}
+
+}  // extern "C"

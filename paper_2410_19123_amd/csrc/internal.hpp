@@ -1,0 +1,42 @@
+// Internal launchers of libreadme (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "readme.h"
+
+namespace readme {
+
+enum GemmEpilogue { EPI_GATE_UP_SILU = 0, EPI_STORE = 1, EPI_RESID_ADD = 2 };
+
+// C = A * B_e^T on the row block of every expert e (see gemm.hip).
+struct GemmArgs {
+    const void* A;            // [T][K] grouped rows
+    int64_t lda;              // elements
+    const void* B;            // expert 0's [N][K]; expert e at + e * b_expert_stride
+    int64_t ldb;              // elements
+    int64_t b_expert_stride;  // elements
+    int64_t N, K;
+    const int32_t* offsets;   // [E+1], device
+    int E;
+    int64_t T;
+    void* C;                  // [T][ldc] output
+    int64_t ldc;              // elements
+    int n_tiles, m_tiles_max; // filled by the launcher
+};
+
+hipError_t launch_route(readme_dtype dt, int64_t T, int64_t d, int E, const void* x,
+                        const void* w, const float* bias, int32_t* ids, float* logits,
+                        hipStream_t s);
+hipError_t launch_group(int64_t T, int E, const int32_t* ids, int32_t* counts, int32_t* offsets,
+                        int32_t* perm, int32_t* inv_perm, hipStream_t s);
+hipError_t launch_move_rows(int64_t nrows, int64_t row_bytes, const void* src, const int32_t* idx,
+                            int64_t src_rows, void* dst, hipStream_t s);
+hipError_t launch_pack(readme_dtype dt, int64_t E, int64_t d, int64_t I, const void* wg,
+                       const void* wu, const void* wd, void* packed, hipStream_t s);
+hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s);
+hipError_t launch_rms_to_bf16(int64_t T, int64_t d, const float* x, const int32_t* offsets, int E,
+                              float eps, uint16_t* xn, hipStream_t s);
+
+}  // namespace readme

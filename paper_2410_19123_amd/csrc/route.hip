@@ -1,0 +1,142 @@
+// Pre-gating router, top-1 (Eq. 2 with K = 1): one expert id per token,
+// computed once ahead of all layers.
+//
+// The argmax decides an integer, so every logit is summed in one fixed fp32
+// order (stated in readme.h): hardware lane l of a wave owns 16-byte chunks
+// l, l + 64, l + 128, ... of the token row and of the router row, fuses
+// multiply-adds over them in ascending k from +0, and the 64 lane partials
+// fold pairwise with offsets 32, 16, 8, 4, 2, 1.  Each wave handles R tokens
+// at once so that one router-row load feeds R tokens; each router row chunk
+// is a coalesced 1 KB wave load.  The path is VALU-bound (fp32 FMA), not
+// MFMA: an MFMA's internal accumulation order is not this order.
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace readme {
+
+template <int W>
+struct Chunk;
+template <>
+struct Chunk<8> {  // 8 bf16
+    __device__ static void load(const void* base, int64_t idx, float* v) {
+        const uint4 q = reinterpret_cast<const uint4*>(base)[idx];
+        v[0] = bf16_lo(q.x); v[1] = bf16_hi(q.x);
+        v[2] = bf16_lo(q.y); v[3] = bf16_hi(q.y);
+        v[4] = bf16_lo(q.z); v[5] = bf16_hi(q.z);
+        v[6] = bf16_lo(q.w); v[7] = bf16_hi(q.w);
+    }
+};
+template <>
+struct Chunk<4> {  // 4 fp32
+    __device__ static void load(const void* base, int64_t idx, float* v) {
+        const float4 q = reinterpret_cast<const float4*>(base)[idx];
+        v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+    }
+};
+
+template <int R, int EB, int W>
+__global__ __launch_bounds__(256) void k_route(int64_t T, int64_t d, int E,
+                                               const void* __restrict__ x,
+                                               const void* __restrict__ wr,
+                                               const float* __restrict__ bias,
+                                               int32_t* __restrict__ ids,
+                                               float* __restrict__ logits) {
+    const int lane = threadIdx.x & 63;
+    const int64_t t0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * R;
+    if (t0 >= T) return;
+    const int64_t nchunks = d / W;  // chunks per row
+
+    int64_t trow[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) trow[r] = (t0 + r < T ? t0 + r : T - 1) * nchunks;
+
+    float best[R];
+    int bid[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) { best[r] = 0.0f; bid[r] = 0; }
+
+    for (int e0 = 0; e0 < E; e0 += EB) {
+        float acc[R][EB];
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int b = 0; b < EB; ++b) acc[r][b] = 0.0f;
+
+        for (int64_t c = lane; c < nchunks; c += 64) {
+            float xv[R][W];
+#pragma unroll
+            for (int r = 0; r < R; ++r) Chunk<W>::load(x, trow[r] + c, xv[r]);
+#pragma unroll
+            for (int b = 0; b < EB; ++b) {
+                if (e0 + b < E) {
+                    float wv[W];
+                    Chunk<W>::load(wr, (int64_t)(e0 + b) * nchunks + c, wv);
+#pragma unroll
+                    for (int r = 0; r < R; ++r)
+#pragma unroll
+                        for (int q = 0; q < W; ++q)
+                            acc[r][b] = __builtin_fmaf(xv[r][q], wv[q], acc[r][b]);
+                }
+            }
+        }
+
+#pragma unroll
+        for (int b = 0; b < EB; ++b) {
+            const int e = e0 + b;
+            if (e >= E) break;
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                float v = acc[r][b];
+#pragma unroll
+                for (int off = 32; off >= 1; off >>= 1) {
+                    const float o = __shfl_down(v, off, 64);
+                    v = v + o;
+                }
+                float logit = __shfl(v, 0, 64);
+                if (bias) logit = logit + bias[e];
+                if (logits && lane == 0 && t0 + r < T) logits[(t0 + r) * E + e] = logit;
+                if (e == 0) {
+                    best[r] = logit;
+                    bid[r] = 0;
+                } else if (logit > best[r]) {
+                    best[r] = logit;
+                    bid[r] = e;
+                }
+            }
+        }
+    }
+    if (lane == 0) {
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            if (t0 + r < T) ids[t0 + r] = bid[r];
+    }
+}
+
+template <int R, int W>
+static hipError_t launch_route_r(int64_t T, int64_t d, int E, const void* x, const void* w,
+                                 const float* bias, int32_t* ids, float* logits,
+                                 hipStream_t s) {
+    const int64_t blocks = ceil_div(T, 4 * R);
+    if (E <= 4)
+        k_route<R, 4, W><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(T, d, E, x, w, bias, ids, logits);
+    else if (E <= 8)
+        k_route<R, 8, W><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(T, d, E, x, w, bias, ids, logits);
+    else
+        k_route<R, 16, W><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(T, d, E, x, w, bias, ids, logits);
+    return hipGetLastError();
+}
+
+hipError_t launch_route(readme_dtype dt, int64_t T, int64_t d, int E, const void* x,
+                        const void* w, const float* bias, int32_t* ids, float* logits,
+                        hipStream_t s) {
+    // Few tokens: one token per wave spreads the work over the chip; many
+    // tokens: four per wave so that one router-row load serves four tokens.
+    const bool many = T >= 8192;
+    if (dt == README_BF16)
+        return many ? launch_route_r<4, 8>(T, d, E, x, w, bias, ids, logits, s)
+                    : launch_route_r<1, 8>(T, d, E, x, w, bias, ids, logits, s);
+    return many ? launch_route_r<4, 4>(T, d, E, x, w, bias, ids, logits, s)
+                : launch_route_r<1, 4>(T, d, E, x, w, bias, ids, logits, s);
+}
+
+}  // namespace readme

@@ -1,0 +1,103 @@
+"""The C-ABI library loads on the CPU, exports every function readme.h
+declares, and rejects bad arguments on the host before any launch (no GPU
+needed: these calls never reach the HIP runtime)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "readme.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(readme_[a-z0-9_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2410_19123_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.skip("libreadme.so not built")
+    return _lib.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_binding_covers_header():
+    from paper_2410_19123_amd import _lib
+    assert set(_declared()) == set(_lib.SIGNATURES)
+
+
+def test_status_strings_and_version(lib):
+    assert lib.readme_abi_version() == 1
+    assert lib.readme_status_string(0) == b"ok"
+    assert lib.readme_status_string(3) == b"buffer smaller than required"
+
+
+def test_sizes(lib):
+    assert lib.readme_padded_intermediate(1376) == 1408
+    assert lib.readme_padded_intermediate(688) == 704
+    assert lib.readme_padded_intermediate(512) == 512
+    assert lib.readme_packed_experts_bytes(1, 8, 4096, 1376) == 8 * 3 * 1408 * 4096 * 2
+    assert lib.readme_packed_experts_bytes(0, 4, 512, 512) == 4 * 3 * 512 * 512 * 4
+    assert lib.readme_packed_experts_bytes(1, 0, 4096, 1376) == 0
+    assert lib.readme_moe_ffn_workspace_bytes(1, 2048, 1376) == 2048 * 1408 * 2
+    assert lib.readme_moe_ffn_stack_workspace_bytes(64, 4096, 1376) == 64 * 4096 * 2 + 64 * 1408 * 2
+
+
+FAKE = ctypes.c_void_p(4096)   # never dereferenced: every call below fails validation
+
+
+def test_route_argument_errors(lib):
+    r = lib.readme_route
+    assert r(7, 4, 64, 2, FAKE, FAKE, None, FAKE, None, None) == 1          # bad dtype
+    assert r(1, -1, 64, 2, FAKE, FAKE, None, FAKE, None, None) == 1         # T < 0
+    assert r(1, 4, 64, 0, FAKE, FAKE, None, FAKE, None, None) == 2          # E < 1
+    assert r(1, 4, 64, 257, FAKE, FAKE, None, FAKE, None, None) == 2        # E > 256
+    assert r(1, 4, 60, 2, FAKE, FAKE, None, FAKE, None, None) == 2          # d % 8
+    assert r(0, 4, 62, 2, FAKE, FAKE, None, FAKE, None, None) == 2          # d % 4 (fp32)
+    assert r(1, 4, 64, 2, None, FAKE, None, FAKE, None, None) == 1          # NULL x
+    assert r(1, 4, 64, 2, ctypes.c_void_p(4100), FAKE, None, FAKE, None, None) == 1  # misaligned
+    assert r(1, 0, 64, 2, None, None, None, None, None, None) == 0          # T = 0: no-op
+
+
+def test_group_argument_errors(lib):
+    g = lib.readme_group_by_expert
+    assert g(-1, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 64, None, None, None) == 1
+    assert g(8, 0, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 64, None, None, None) == 2
+    assert g(8, 4, None, FAKE, FAKE, FAKE, FAKE, 1, 64, None, None, None) == 1
+    assert g(8, 4, FAKE, FAKE, FAKE, FAKE, None, 1, 64, None, None, None) == 1
+    assert g(8, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 64, FAKE, None, None) == 1   # half a gather
+    assert g(8, 4, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 4, FAKE, FAKE, None) == 2    # 8-byte rows
+
+
+def test_ffn_argument_errors(lib):
+    f = lib.readme_moe_ffn
+    assert f(1, 16, 4096, 8, 1376, FAKE, FAKE, FAKE, FAKE, FAKE, 10, None) == 3  # workspace
+    assert f(1, 16, 4000, 8, 1376, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 2
+    assert f(1, 16, 4096, 8, 0, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 1
+    assert f(1, 16, 4096, 300, 16, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 2
+    assert f(1, 16, 4096, 8, 16, None, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 1
+    assert f(1, 0, 4096, 8, 16, None, None, None, None, None, 0, None) == 0
+    p = lib.readme_pack_experts
+    assert p(1, 8, 4096, 1376, FAKE, FAKE, FAKE, FAKE, 100, None) == 3
+    assert p(1, 8, 4096, 1376, FAKE, None, FAKE, FAKE, 1 << 40, None) == 1
+    u = lib.readme_ungroup
+    assert u(1, 8, 4, FAKE, FAKE, FAKE, None) == 2
+    assert u(1, 8, 64, FAKE, None, FAKE, None) == 1
+    s = lib.readme_moe_ffn_stack
+    arr = (ctypes.c_void_p * 1)(4096)
+    assert s(64, 4096, 8, 1376, 1, arr, FAKE, FAKE, ctypes.c_float(-1.0), FAKE, 1 << 40,
+             None) == 1
+    assert s(64, 4096, 8, 1376, 1, arr, FAKE, FAKE, ctypes.c_float(1e-5), FAKE, 10, None) == 3
+    assert s(64, 4096, 8, 1376, -1, arr, FAKE, FAKE, ctypes.c_float(1e-5), FAKE, 1 << 40,
+             None) == 1

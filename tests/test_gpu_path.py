@@ -1,0 +1,271 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Integer results (expert ids, counts, offsets, perm, inv_perm, moved rows) and
+the router's fp32 logits must be bit-exact; FFN outputs must meet the
+tolerance in tests/_util.py.  Full-size workloads are checked on sampled rows
+that include every expert block's edges.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2410_19123_amd import workloads as wl
+
+from . import _util as U
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    from paper_2410_19123_amd import _lib
+    _lib.load()
+    return _lib
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+# ------------------------------------------------------------------ route
+@pytest.mark.parametrize("name", ["tiny_f32", "llama7b_layer", "llama7b_decode32",
+                                  "prefill_skew16"])
+def test_route_bit_exact(L, oracle_mod, name):
+    w = wl.WORKLOADS[name]
+    _say("route", name)
+    x = wl.make_x(w)
+    wr, b = wl.make_router(w)
+    ids_ref, lg_ref = oracle_mod.route(x, wr, b)
+    logits = torch.empty(w.T, w.E, dtype=torch.float32, device=U.dev())
+    ids, _ = L.readme_route(U.to_dev(x), U.to_dev(wr), None if b is None else U.to_dev(b),
+                            logits=logits)
+    torch.cuda.synchronize()
+    assert (U.from_dev(ids) == ids_ref).all()
+    assert (U.from_dev(logits).view(np.uint32) == lg_ref.view(np.uint32)).all()
+
+
+@pytest.mark.parametrize("T,d,E,dtype", [(1, 8, 1, "bf16"), (5, 24, 3, "bf16"),
+                                         (70, 4, 2, "f32"), (300, 520, 37, "bf16"),
+                                         (9000, 256, 16, "bf16"), (130, 1032, 256, "bf16")])
+def test_route_odd_shapes_and_ties(L, oracle_mod, T, d, E, dtype):
+    w = wl.Workload("t", T=T, d=d, E=E, I=8, dtype=dtype, bias="zipf1")
+    _say("route shape", T, d, E, dtype)
+    x = wl.make_x(w, 2)
+    wr, b = wl.make_router(w, 2)
+    if E >= 3:
+        wr = wr.copy()
+        wr[E - 1] = wr[1]          # exact tie between e=1 and e=E-1
+        b = b.copy()
+        b[E - 1] = b[1]
+    ids_ref, lg_ref = oracle_mod.route(x, wr, b)
+    logits = torch.empty(T, E, dtype=torch.float32, device=U.dev())
+    ids, _ = L.readme_route(U.to_dev(x), U.to_dev(wr), U.to_dev(b), logits=logits)
+    torch.cuda.synchronize()
+    assert (U.from_dev(ids) == ids_ref).all()
+    assert (U.from_dev(logits).view(np.uint32) == lg_ref.view(np.uint32)).all()
+
+
+# ------------------------------------------------------------------ group
+def _ids_case(kind, T, E, seed):
+    rng = np.random.default_rng(seed)
+    if kind == "uniform":
+        return rng.integers(0, E, size=T).astype(np.int32)
+    if kind == "one_expert":
+        return np.full(T, E - 1, np.int32)
+    if kind == "empty_ends":          # first and last experts empty
+        return rng.integers(1, max(E - 1, 2), size=T).astype(np.int32) % E
+    if kind == "invalid":             # some ids outside [0, E)
+        ids = rng.integers(-2, E + 2, size=T).astype(np.int32)
+        return ids
+    if kind == "local":               # each token repeats its predecessor w.p. 0.713
+        ids = np.empty(T, np.int32)
+        cur = 0
+        for t in range(T):
+            if t == 0 or rng.random() >= 0.713:
+                cur = int(rng.integers(0, E))
+            ids[t] = cur
+        return ids
+    raise ValueError(kind)
+
+
+@pytest.mark.parametrize("kind,T,E", [
+    ("uniform", 1, 1), ("uniform", 63, 4), ("uniform", 65, 4), ("uniform", 1024, 8),
+    ("uniform", 1025, 8), ("uniform", 16384, 16), ("uniform", 5000, 256),
+    ("one_expert", 3000, 8), ("empty_ends", 2048, 8), ("invalid", 2500, 7),
+    ("local", 4096, 8), ("uniform", 40000, 3), ("uniform", 0, 4)])
+def test_group_bit_exact(L, oracle_mod, kind, T, E):
+    _say("group", kind, T, E)
+    ids = _ids_case(kind, T, E, seed=T + E)
+    d = 64
+    x = np.random.default_rng(1).integers(0, 65535, size=(T, d)).astype(np.uint16)
+    counts_ref, off_ref, perm_ref, inv_ref = oracle_mod.group(ids, E)
+    xg_ref = oracle_mod.gather(x, perm_ref) if T else x
+    xd = U.to_dev(x) if T else torch.empty(0, d, dtype=torch.bfloat16, device=U.dev())
+    counts, offs, perm, inv, xg = L.readme_group_by_expert(
+        U.to_dev(ids) if T else torch.empty(0, dtype=torch.int32, device=U.dev()), E, x=xd)
+    torch.cuda.synchronize()
+    assert (U.from_dev(counts) == counts_ref).all()
+    assert (U.from_dev(offs) == off_ref).all()
+    if T:
+        assert (U.from_dev(perm) == perm_ref).all()
+        assert (U.from_dev(inv) == inv_ref).all()
+        assert (U.from_dev(xg) == xg_ref).all()
+        # And back: ungroup of the grouped rows restores routed tokens.
+        y = L.readme_ungroup(xg, inv)
+        torch.cuda.synchronize()
+        assert (U.from_dev(y) == oracle_mod.ungroup(xg_ref, inv_ref)).all()
+
+
+# -------------------------------------------------------------------- ffn
+def _run_ffn(L, x_g, offsets, wg, wu, wd, E, I):
+    packed = L.readme_pack_experts(*U.weights_to_dev(wg, wu, wd))
+    y = L.readme_moe_ffn(U.to_dev(x_g), U.to_dev(offsets), packed, E, I)
+    torch.cuda.synchronize()
+    return U.from_dev(y), packed
+
+
+@pytest.mark.parametrize("dtype,d,I,counts", [
+    ("bf16", 256, 96, [0, 1, 31, 32, 33, 0]),
+    ("bf16", 128, 40, [127, 128, 129, 255, 256, 257]),
+    ("bf16", 64, 688, [5, 0, 300, 1]),
+    ("f32", 128, 72, [0, 17, 128, 129, 3]),
+    ("bf16", 512, 64, [800, 0, 0, 770]),
+    ("bf16", 192, 130, [1]),
+])
+def test_ffn_ragged_blocks(L, oracle_mod, dtype, d, I, counts):
+    E = len(counts)
+    T = sum(counts)
+    _say("ffn ragged", dtype, d, I, counts)
+    w = wl.Workload("t", T=T, d=d, E=E, I=I, dtype=dtype)
+    x = wl.make_x(w, 3)
+    wg, wu, wd = wl.make_experts(w, 3)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    y, _ = _run_ffn(L, x, offsets, wg, wu, wd, E, I)
+    ref = oracle_mod.moe_ffn(x, offsets, wg, wu, wd)
+    U.close(y, ref, f"ffn {counts}")
+
+
+def test_gate_up_pad_columns_are_zero(L, oracle_mod):
+    w = wl.Workload("t", T=100, d=128, E=2, I=40, dtype="bf16")
+    x = wl.make_x(w, 4)
+    wg, wu, wd = wl.make_experts(w, 4)
+    offsets = np.array([0, 60, 100], np.int32)
+    packed = L.readme_pack_experts(*U.weights_to_dev(wg, wu, wd))
+    h = L.readme_moe_gate_up(U.to_dev(x), U.to_dev(offsets), packed, 2, 40)
+    torch.cuda.synchronize()
+    hh = U.from_dev(h)
+    assert hh.shape == (100, 64)
+    assert (hh[:, 40:] == 0).all()
+    # h itself against fp64: silu(W_g x) * (W_u x).
+    xf = U.as_f64(x)
+    for e, (a, b) in enumerate([(0, 60), (60, 100)]):
+        g = xf[a:b] @ U.as_f64(wg[e]).T
+        u = xf[a:b] @ U.as_f64(wu[e]).T
+        ref = g / (1 + np.exp(-g)) * u
+        U.close(hh[a:b, :40], ref, "h")
+
+
+# ------------------------------------------------------------- full path
+def _full_path(L, w, x, wr, b, ids_given, wg, wu, wd):
+    xd = U.to_dev(x)
+    if ids_given is None:
+        ids, _ = L.readme_route(xd, U.to_dev(wr), None if b is None else U.to_dev(b))
+    else:
+        ids = U.to_dev(ids_given)
+    counts, offs, perm, inv, xg = L.readme_group_by_expert(ids, w.E, x=xd)
+    packed = L.readme_pack_experts(*U.weights_to_dev(wg, wu, wd))
+    yg = L.readme_moe_ffn(xg, offs, packed, w.E, w.I)
+    y = L.readme_ungroup(yg, inv)
+    torch.cuda.synchronize()
+    return dict(ids=U.from_dev(ids), counts=U.from_dev(counts), offsets=U.from_dev(offs),
+                perm=U.from_dev(perm), inv=U.from_dev(inv), x_g=U.from_dev(xg),
+                y_g=U.from_dev(yg), y=U.from_dev(y))
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "llama7b_layer", "prefill_skew16",
+                                  "wide_requests"])
+def test_full_path_workloads(L, oracle_mod, name):
+    w = wl.WORKLOADS[name]
+    _say("full path", name)
+    x = wl.make_x(w)
+    wr, b = wl.make_router(w)
+    ids_given = None if w.router else wl.make_request_ids(w)
+    wg, wu, wd = wl.make_experts(w)
+    got = _full_path(L, w, x, wr, b, ids_given, wg, wu, wd)
+    ids_ref = ids_given if ids_given is not None else oracle_mod.route(x, wr, b)[0]
+    counts, offsets, perm, inv = oracle_mod.group(ids_ref, w.E)
+    assert (got["ids"] == ids_ref).all()
+    assert (got["counts"] == counts).all() and (got["offsets"] == offsets).all()
+    assert (got["perm"] == perm).all() and (got["inv"] == inv).all()
+    x_g = oracle_mod.gather(x, perm)
+    assert (got["x_g"] == x_g).all()
+    if w.T <= 256:
+        rows = np.arange(w.T)
+    else:
+        rows = U.sample_rows(offsets, 96 if w.d > 4096 else 192)
+    ref = oracle_mod.moe_ffn(x_g, offsets, wg, wu, wd, rows=rows)
+    U.close(got["y_g"][rows], ref, name)
+    # Ungroup is a row move: y[t] == y_g[inv[t]] bit for bit.
+    assert (got["y"] == got["y_g"][inv]).all()
+
+
+def test_deterministic_bitwise(L):
+    w = wl.WORKLOADS["llama7b_layer"]
+    x = wl.make_x(w)
+    wr, b = wl.make_router(w)
+    wg, wu, wd = wl.make_experts(w)
+    a = _full_path(L, w, x, wr, b, None, wg, wu, wd)
+    c = _full_path(L, w, x, wr, b, None, wg, wu, wd)
+    for k in a:
+        assert (a[k] == c[k]).all(), k
+
+
+def test_single_expert_equals_dense_ffn(L, oracle_mod):
+    # E = 1 with the full dense width: the MoE layer is the dense SwiGLU FFN.
+    w = wl.Workload("t", T=300, d=512, E=1, I=1376, dtype="bf16")
+    x = wl.make_x(w, 8)
+    wg, wu, wd = wl.make_experts(w, 8)
+    offsets = np.array([0, 300], np.int32)
+    y, _ = _run_ffn(L, x, offsets, wg, wu, wd, 1, 1376)
+    dg, du, dd = wl.make_dense(w, 8)
+    xf = U.as_f64(x)
+    g = xf @ U.as_f64(dg).T
+    u = xf @ U.as_f64(du).T
+    ref = (g / (1 + np.exp(-g)) * u) @ U.as_f64(dd).T
+    U.close(y, ref, "dense")
+
+
+# ------------------------------------------------------------ decode stack
+def test_decode_stack_teacher_forced(L, oracle_mod):
+    w = wl.WORKLOADS["llama7b_decode32"]
+    _say("decode stack")
+    x = wl.make_x(w)
+    wr, b = wl.make_router(w)
+    ids, _ = L.readme_route(U.to_dev(x), U.to_dev(wr), U.to_dev(b))
+    counts, offs, perm, inv, xg = L.readme_group_by_expert(ids, w.E, x=U.to_dev(x))
+    offsets = U.from_dev(offs)
+    layers = [0, 1, 2, 31]
+    packed, host = {}, {}
+    for l in layers:
+        host[l] = wl.make_experts(w, 0, layer=l)
+        packed[l] = L.readme_pack_experts(*U.weights_to_dev(*host[l]))
+    xr = xg.float()
+    for l in layers:
+        x_in = xr.clone()
+        L.readme_moe_ffn_stack(xr, offs, [packed[l]], w.E, w.I)
+        torch.cuda.synchronize()
+        xin = U.from_dev(x_in)
+        delta = U.from_dev(xr).astype(np.float64) - xin.astype(np.float64)
+        ref = oracle_mod.layer(xin, offsets, *host[l], eps=1e-5)
+        U.close(delta, ref, f"layer {l}")
+    # One call over several layers equals the chain of single-layer calls.
+    xa = xg.float()
+    L.readme_moe_ffn_stack(xa, offs, [packed[l] for l in layers], w.E, w.I)
+    torch.cuda.synchronize()
+    assert (U.from_dev(xa) == U.from_dev(xr)).all()
+    # Ungroup of the fp32 residual stream back to token order.
+    y = L.readme_ungroup(xa, inv)
+    torch.cuda.synchronize()
+    assert (U.from_dev(y) == U.from_dev(xa)[U.from_dev(inv)]).all()
