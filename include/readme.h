@@ -152,6 +152,18 @@ readme_status readme_pack_experts(readme_dtype dt, int32_t E, int64_t d,
 int64_t readme_padded_intermediate(int64_t I);
 
 /*
+ * readme_set_gemm_tile -- choose the workgroup tile of the grouped GEMMs,
+ * process-wide, for tuning and for testing every configuration.
+ *   0 = automatic (by tokens per expert, the default)
+ *   1 = 256x256, 2 = 256x128, 3 = 128x128, 4 = 128x256, 5 = 64x128,
+ *   6 = 32x128  (rows of tokens x columns of outputs)
+ * Results do not depend on the tile beyond fp32 summation order.  Returns
+ * README_ERR_ARG for any other value.  Not synchronised with calls in
+ * flight on other host threads.
+ */
+readme_status readme_set_gemm_tile(int32_t tile);
+
+/*
  * readme_moe_ffn -- each expert's SwiGLU FFN on its token block (Eq. 2 with
  * a fixed top-1 expert; the output is the expert's, unweighted).
  *

@@ -366,3 +366,11 @@ void oracle_f32_to_bf16(int64_t n, const float *src, uint16_t *dst)
     for (int64_t i = 0; i < n; ++i)
         dst[i] = float_to_bf16_bits(src[i]);
 }
+
+/* Threads the OpenMP loops above use (reported beside oracle timings). */
+#ifdef _OPENMP
+#include <omp.h>
+int oracle_threads(void) { return omp_get_max_threads(); }
+#else
+int oracle_threads(void) { return 1; }
+#endif

@@ -53,6 +53,8 @@ def _load():
                                           ctypes.c_float, I64, P, P, P]
         lib.oracle_f32_to_bf16.argtypes = [I64, P, P]
         lib.oracle_f32_to_bf16.restype = None
+        lib.oracle_threads.argtypes = []
+        lib.oracle_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -166,6 +168,11 @@ def layer(x_res, offsets, w_gate, w_up, w_down, eps=1e-5, rows=None,
         _p(np.ascontiguousarray(w_down, dtype=np.uint16)),
         float(eps), n, _p(r), _p(y), _p(xn)), "layer")
     return (y, xn) if want_xn else y
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(_load().oracle_threads())
 
 
 def f32_to_bf16(a: np.ndarray) -> np.ndarray:

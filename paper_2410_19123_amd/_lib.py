@@ -34,6 +34,7 @@ SIGNATURES = {
     "readme_packed_experts_bytes": (_SZ, [_I32, _I32, _I64, _I64]),
     "readme_pack_experts": (_I32, [_I32, _I32, _I64, _I64, _P, _P, _P, _P, _SZ, _P]),
     "readme_padded_intermediate": (_I64, [_I64]),
+    "readme_set_gemm_tile": (_I32, [_I32]),
     "readme_moe_ffn_workspace_bytes": (_SZ, [_I32, _I64, _I64]),
     "readme_moe_ffn": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _SZ, _P]),
     "readme_moe_gate_up": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P]),
@@ -138,6 +139,11 @@ def readme_group_by_expert(expert_ids, E, x=None, counts=None, offsets=None, per
 
 def readme_padded_intermediate(I: int) -> int:
     return int(load().readme_padded_intermediate(I))
+
+
+def readme_set_gemm_tile(tile: int) -> None:
+    """Force a grouped-GEMM tile configuration (0 = automatic)."""
+    _call("readme_set_gemm_tile", tile)
 
 
 def readme_packed_experts_bytes(dtype, E, d, I) -> int:

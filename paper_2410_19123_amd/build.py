@@ -32,9 +32,19 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
+# Per-source extra flags.  The grouped GEMM asks LLVM's AMDGPU machine
+# scheduler for its iterative ILP strategy, which keeps the next k-slice's
+# LDS fragment reads in flight under the current slice's MFMAs (the default
+# strategy shortens register live ranges by loading each fragment just
+# before its first use, which stalls a one-wave-per-SIMD kernel).
+EXTRA = {
+    "gemm.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"],
+}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(OBJ_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")

@@ -82,6 +82,10 @@ int32_t readme_abi_version(void) { return 1; }
 
 int64_t readme_padded_intermediate(int64_t I) { return I < 1 ? 0 : padded_I(I); }
 
+readme_status readme_set_gemm_tile(int32_t tile) {
+    return set_gemm_tile(tile) ? README_OK : README_ERR_ARG;
+}
+
 readme_status readme_route(readme_dtype dt, int64_t T, int64_t d, int32_t E, const void* x,
                            const void* w_router, const float* bias, int32_t* expert_ids,
                            float* logits, void* stream) {

@@ -12,44 +12,94 @@
 //
 // Tiling.  A workgroup owns a BM x BN output tile of one expert; each of its
 // WGM x WGN waves owns a (BM/WGM) x (BN/WGN) sub-tile made of 32x32 MFMA
-// tiles (v_mfma_f32_32x32x16_bf16, or 4 x v_mfma_f32_32x32x2_f32 for fp32,
-// both consuming one 16-byte fragment per lane and operand).  A K-step moves
-// 128 bytes of every A and B row through LDS (64 bf16 / 32 fp32), double
-// buffered; 16-byte chunks are XOR-swizzled by row (chunk c of row r sits in
-// slot c ^ (r & 7)) so that the 32 rows a fragment load touches spread over
-// all LDS banks.
+// tiles (v_mfma_f32_32x32x16_bf16, or 4 x v_mfma_f32_32x32x2_f32 for fp32;
+// both consume one 16-byte fragment per lane and operand, and the two
+// operands use the same k order inside a fragment, so the product is exact
+// whatever order the unit sums in).
+//
+// Data movement.  A K-step moves CPR 16-byte chunks of every A and B row
+// (CPR = 8: 128 bytes = 64 bf16 / 32 fp32; CPR = 4: 64 bytes) straight from
+// global memory into LDS with global_load_lds_dwordx4 (no VGPR staging).
+// One such wave instruction fills 1 KB of LDS = 1024 / (16 CPR) rows.  A
+// 16-byte fragment read serves 16 lanes = 16 consecutive rows per LDS cycle
+// over 64 four-byte banks, and a row covers 4 CPR of them, so the 16 rows
+// must land on 16 distinct 16-byte bank groups: chunk c of row r is stored
+// in slot c ^ ((r / (8 / CPR)) % CPR) -- for CPR = 8, rows alternate bank
+// halves and the XOR spreads each parity class; for CPR = 4, rows cycle
+// through four quarters and the XOR spreads each class.  The swizzle is
+// applied on the global side by choosing which chunk each lane fetches.
+// NSTAGE K-steps are in flight: at step kt the workgroup waits for stage kt
+// (s_waitcnt vmcnt counts this wave's later stages), meets at one barrier,
+// refills the buffer freed by step kt-1 with step kt+NSTAGE-1, then runs
+// step kt's MFMAs with fragments double-buffered in registers.  The barrier
+// is a bare s_barrier: the DMA completion is covered by the explicit vmcnt
+// wait, so the compiler's conservative full wait is not needed.
 //
 // Scheduling.  The number of M tiles per expert is only known on the device,
 // so the grid is launched for an upper bound, sum_e ceil(T_e/BM) <=
-// (T + E*(BM-1)) / BM, and each workgroup finds its expert by scanning the
-// device offsets; workgroups past the last tile exit at once.  Workgroups are
-// dealt to the 8 XCDs round-robin by the dispatcher; the linear tile index is
-// remapped so that each XCD receives a contiguous run of tiles, M fastest:
-// the M tiles that share one expert's weight tile run on the same XCD and
-// share its L2.
+// (T + E*(BM-1)) / BM, times the N tiles, and each workgroup finds its tile
+// by scanning the device offsets; workgroups past the last tile exit at
+// once.  Workgroups are dealt to the 8 XCDs round-robin by the dispatcher;
+// the linear tile index is remapped so that each XCD receives a contiguous
+// run of tiles.  Within one expert the run walks groups of up to GROUP_M
+// M tiles: for each N tile, the group's M tiles, so that the workgroups an
+// XCD runs together share both their activation rows (across N tiles) and
+// their weight rows (across the group) in that XCD's L2.
 #include "common.hpp"
 #include "internal.hpp"
 
 namespace readme {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+#define LDS_AS __attribute__((address_space(3)))
 
-template <int BM, int BN, int WGM, int WGN, bool F32, int EPI>
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// One 16-byte global -> LDS transfer per lane; the LDS address is the
+// wave-uniform `lds` plus 16 * lane.  (Kept out of lambdas: the host pass of
+// a kernel drops its launch stub if a lambda in it names this builtin.)
+__device__ __forceinline__ void dma16(const char* gsrc, u32x4* lds) {
+    __builtin_amdgcn_global_load_lds(gsrc, (LDS_AS void*)lds, 16, 0, 0);
+}
+
+__device__ __forceinline__ void block_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+constexpr int GROUP_M = 4;
+
+// LDS slot of logical chunk c of tile row r (see the bank analysis above).
+template <int CPR>
+__device__ __forceinline__ int swz(int c, int r) {
+    return c ^ ((r / (8 / CPR)) % CPR);
+}
+
+template <int BM, int BN, int WGM, int WGN, int NSTAGE, int CPR, bool F32, int EPI>
 __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
-    constexpr int NT = WGM * WGN * 64;
+    constexpr int NW = WGM * WGN;
     constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int TM = WM / 32, TN = WN / 32;
-    constexpr int CPR = 8;                 // 16-byte chunks per row per K-step
+    constexpr int RPI = 64 / CPR;          // tile rows per DMA instruction
     constexpr int EPC = F32 ? 4 : 8;       // elements per chunk
     constexpr int BK = CPR * EPC;          // K elements per step
     constexpr int ESZ = F32 ? 4 : 2;
-    constexpr int A_LD = BM * CPR / NT;    // chunk loads per thread
-    constexpr int B_LD = BN * CPR / NT;
+    constexpr int A_INS = BM / RPI / NW;   // DMA instructions per wave per stage
+    constexpr int B_INS = BN / RPI / NW;
+    constexpr int LPS = A_INS + B_INS;
+    constexpr int STAGE = (BM + BN) * CPR; // u32x4 slots per stage
     static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile");
-    static_assert(A_LD * NT == BM * CPR && B_LD * NT == BN * CPR, "load split");
+    static_assert(CPR == 4 || CPR == 8, "chunks per row");
+    static_assert(A_INS * RPI * NW == BM && B_INS * RPI * NW == BN, "DMA split");
     static_assert(EPI != EPI_GATE_UP_SILU || WN % 64 == 0, "gate/up pairs");
+    static_assert(NSTAGE >= 2 && LPS * (NSTAGE - 2) < 64, "stages");
 
-    __shared__ u32x4 lds[2][(BM + BN) * CPR];
+    __shared__ u32x4 lds[NSTAGE * STAGE];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -60,57 +110,75 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     const int nb = gridDim.x;
     const int bid = blockIdx.x;
     const int L = (bid & 7) * (nb >> 3) + (bid >> 3);
-    const int n_tile = L / g.m_tiles_max;
-    const int mt = L - n_tile * g.m_tiles_max;
-    if (n_tile >= g.n_tiles) return;
 
-    int e = -1;
+    // Find (expert, M tile, N tile) of L: experts in order, each expert's
+    // tiles in groups of GROUP_M M tiles, N tiles outer, M tiles inner.
+    int e = -1, n_tile = 0;
     int64_t m0 = 0;
     int rows = 0;
     {
-        int acc = 0;
-        int64_t prev = 0;
+        int64_t acc = 0, prev = 0;
+        const int nt_n = g.n_tiles;
         for (int ee = 0; ee < g.E; ++ee) {
             int64_t s = g.offsets[ee], en = g.offsets[ee + 1];
             s = s < prev ? prev : (s > g.T ? g.T : s);
             en = en < s ? s : (en > g.T ? g.T : en);
             prev = en;
-            const int nt = (int)((en - s + BM - 1) / BM);
-            if (mt < acc + nt) {
+            const int mt_e = (int)((en - s + BM - 1) / BM);
+            const int64_t tiles = (int64_t)mt_e * nt_n;
+            if (L < acc + tiles) {
+                const int local = (int)(L - acc);
+                const int grp = local / (GROUP_M * nt_n);
+                const int gm = min(GROUP_M, mt_e - grp * GROUP_M);
+                const int within = local - grp * GROUP_M * nt_n;
+                n_tile = within / gm;
+                const int mt = grp * GROUP_M + (within - n_tile * gm);
                 e = ee;
-                m0 = s + (int64_t)(mt - acc) * BM;
+                m0 = s + (int64_t)mt * BM;
                 rows = (int)((en - m0) < BM ? (en - m0) : BM);
                 break;
             }
-            acc += nt;
+            acc += tiles;
         }
     }
     if (e < 0) return;
     const int64_t n0 = (int64_t)n_tile * BN;
 
-    // Global chunk pointers of this thread's loads (row clamped in bounds;
-    // rows past the expert's block are loaded and never stored).
+    // This lane's DMA sources.  Instruction i of this wave fills tile rows
+    // r = RPI*(wave + NW*i) + lane/CPR, slot lane%CPR, which holds the
+    // logical chunk swz(lane%CPR, r) (an XOR: its own inverse).  Rows are
+    // clamped in bounds; rows past the expert's block are fetched and never
+    // stored.
+    const int rsub = lane / CPR;
     const char* Ab = reinterpret_cast<const char*>(g.A);
     const char* Bb = reinterpret_cast<const char*>(g.B) + (int64_t)e * g.b_expert_stride * ESZ;
-    const u32x4* a_src[A_LD];
-    const u32x4* b_src[B_LD];
-    int a_dst[A_LD], b_dst[B_LD];
+    const char* a_src[A_INS];
+    const char* b_src[B_INS];
 #pragma unroll
-    for (int i = 0; i < A_LD; ++i) {
-        const int q = tid + i * NT, r = q / CPR, c = q % CPR;
+    for (int i = 0; i < A_INS; ++i) {
+        const int r = RPI * (wave + NW * i) + rsub;
         int64_t row = m0 + r;
         row = row < g.T ? row : g.T - 1;
-        a_src[i] = reinterpret_cast<const u32x4*>(Ab + (row * g.lda) * ESZ) + c;
-        a_dst[i] = r * CPR + (c ^ (r & 7));
+        a_src[i] = Ab + row * g.lda * ESZ + swz<CPR>(lane % CPR, r) * 16;
     }
 #pragma unroll
-    for (int i = 0; i < B_LD; ++i) {
-        const int q = tid + i * NT, r = q / CPR, c = q % CPR;
+    for (int i = 0; i < B_INS; ++i) {
+        const int r = RPI * (wave + NW * i) + rsub;
         int64_t row = n0 + r;
         row = row < g.N ? row : g.N - 1;
-        b_src[i] = reinterpret_cast<const u32x4*>(Bb + (row * g.ldb) * ESZ) + c;
-        b_dst[i] = BM * CPR + r * CPR + (c ^ (r & 7));
+        b_src[i] = Bb + row * g.ldb * ESZ + swz<CPR>(lane % CPR, r) * 16;
     }
+
+    auto issue = [&](int stage, int kt) {
+        u32x4* base = lds + stage * STAGE;
+        const int64_t koff = (int64_t)kt * (CPR * 16);
+#pragma unroll
+        for (int i = 0; i < A_INS; ++i)
+            dma16(a_src[i] + koff, base + RPI * (wave + NW * i) * CPR);
+#pragma unroll
+        for (int i = 0; i < B_INS; ++i)
+            dma16(b_src[i] + koff, base + (BM + RPI * (wave + NW * i)) * CPR);
+    };
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -121,63 +189,58 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     const int nk = (int)(g.K / BK);
-    u32x4 ra[A_LD], rb[B_LD];
 #pragma unroll
-    for (int i = 0; i < A_LD; ++i) ra[i] = a_src[i][0];
-#pragma unroll
-    for (int i = 0; i < B_LD; ++i) rb[i] = b_src[i][0];
-#pragma unroll
-    for (int i = 0; i < A_LD; ++i) lds[0][a_dst[i]] = ra[i];
-#pragma unroll
-    for (int i = 0; i < B_LD; ++i) lds[0][b_dst[i]] = rb[i];
-    __syncthreads();
+    for (int s = 0; s < NSTAGE - 1; ++s)
+        if (s < nk) issue(s, s);
 
     const int frow = lane & 31;   // fragment row within a 32-row tile
-    const int fhalf = lane >> 5;  // which chunk of the pair
+    const int fhalf = lane >> 5;  // which chunk of the k-pair
+    const int a_row0 = (wm * WM + frow) * CPR;
+    const int b_row0 = (BM + wn * WN + frow) * CPR;
+
     for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            const int64_t step = (int64_t)(kt + 1) * CPR;  // in chunks
+        if (kt + NSTAGE - 2 < nk)
+            wait_vmcnt<LPS * (NSTAGE - 2)>();
+        else
+            wait_vmcnt<0>();
+        block_barrier();
+        if (kt + NSTAGE - 1 < nk) issue((kt + NSTAGE - 1) % NSTAGE, kt + NSTAGE - 1);
+
+        const u32x4* S = lds + (kt % NSTAGE) * STAGE;
+        u32x4 af[2][TM], bfr[2][TN];
+        auto frag = [&](int buf, int kk) {
+            const int ch = swz<CPR>(2 * kk + fhalf, frow);
 #pragma unroll
-            for (int i = 0; i < A_LD; ++i) ra[i] = a_src[i][step];
+            for (int i = 0; i < TM; ++i) af[buf][i] = S[a_row0 + i * 32 * CPR + ch];
 #pragma unroll
-            for (int i = 0; i < B_LD; ++i) rb[i] = b_src[i][step];
-        }
-        const u32x4* As = &lds[cur][0];
-        const u32x4* Bs = &lds[cur][BM * CPR];
+            for (int j = 0; j < TN; ++j) bfr[buf][j] = S[b_row0 + j * 32 * CPR + ch];
+        };
+        frag(0, 0);
 #pragma unroll
         for (int kk = 0; kk < CPR / 2; ++kk) {
-            const int ch = (2 * kk + fhalf) ^ (frow & 7);
-            u32x4 af[TM], bfr[TN];
+            if (kk + 1 < CPR / 2) frag((kk + 1) & 1, kk + 1);
+            const int cb = kk & 1;
 #pragma unroll
-            for (int i = 0; i < TM; ++i) af[i] = As[(wm * WM + i * 32 + frow) * CPR + ch];
-#pragma unroll
-            for (int j = 0; j < TN; ++j) bfr[j] = Bs[(wn * WN + j * 32 + frow) * CPR + ch];
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
+            for (int i = 0; i < TM; ++i) {
+                // 32-row sub-tiles wholly past the expert's last row do no
+                // MFMA work (wave-uniform branch; their rows are never stored).
+                if (wm * WM + i * 32 >= rows) continue;
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
                     if constexpr (F32) {
 #pragma unroll
                         for (int q = 0; q < 4; ++q)
                             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(
-                                __uint_as_float(af[i][q]), __uint_as_float(bfr[j][q]), acc[i][j],
-                                0, 0, 0);
+                                __uint_as_float(af[cb][i][q]), __uint_as_float(bfr[cb][j][q]),
+                                acc[i][j], 0, 0, 0);
                     } else {
                         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            __builtin_bit_cast(bf16x8, af[i]), __builtin_bit_cast(bf16x8, bfr[j]),
-                            acc[i][j], 0, 0, 0);
+                            __builtin_bit_cast(bf16x8, af[cb][i]),
+                            __builtin_bit_cast(bf16x8, bfr[cb][j]), acc[i][j], 0, 0, 0);
                     }
                 }
+            }
         }
-        if (more) {
-#pragma unroll
-            for (int i = 0; i < A_LD; ++i) lds[cur ^ 1][a_dst[i]] = ra[i];
-#pragma unroll
-            for (int i = 0; i < B_LD; ++i) lds[cur ^ 1][b_dst[i]] = rb[i];
-        }
-        __syncthreads();
     }
 
     // Epilogue.  32x32 accumulator layout: register r of lane l holds row
@@ -195,8 +258,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
                 for (int j = 0; j < TN; j += 2) {
                     const int64_t nb0 = n0 + wn * WN + j * 32;  // gate group start
                     if (nb0 >= g.N) continue;
-                    const float gv = acc[i][j][r], uv = acc[i][j + 1][r];
-                    const float h = silu_f32(gv) * uv;
+                    const float h = silu_f32(acc[i][j][r]) * acc[i][j + 1][r];
                     const int64_t hc = nb0 / 2 + col;
                     if constexpr (F32)
                         reinterpret_cast<float*>(g.C)[grow * g.ldc + hc] = h;
@@ -206,8 +268,8 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
             } else {
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
-                    const int64_t c = n0 + wn * WN + j * 32 + col;
                     if (n0 + wn * WN + j * 32 >= g.N) continue;
+                    const int64_t c = n0 + wn * WN + j * 32 + col;
                     const float v = acc[i][j][r];
                     if constexpr (EPI == EPI_RESID_ADD) {
                         float* y = reinterpret_cast<float*>(g.C) + grow * g.ldc + c;
@@ -223,7 +285,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     }
 }
 
-template <int BM, int BN, int WGM, int WGN, bool F32, int EPI>
+template <int BM, int BN, int WGM, int WGN, int NSTAGE, int CPR, bool F32, int EPI>
 static hipError_t launch_cfg(GemmArgs g, hipStream_t s) {
     g.n_tiles = (int)ceil_div(g.N, BN);
     int64_t mt = (g.T + (int64_t)g.E * (BM - 1)) / BM;
@@ -232,20 +294,60 @@ static hipError_t launch_cfg(GemmArgs g, hipStream_t s) {
     const int64_t blocks = round_up((int64_t)g.n_tiles * g.m_tiles_max, 8);
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    k_grouped_gemm<BM, BN, WGM, WGN, F32, EPI>
+    k_grouped_gemm<BM, BN, WGM, WGN, NSTAGE, CPR, F32, EPI>
         <<<dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, s>>>(g);
     return hipGetLastError();
 }
 
+// Tile configurations: workgroup tile, wave grid (wave tile), K-stages in
+// flight x bytes per row per stage, LDS.  readme_set_gemm_tile() forces one
+// process-wide.
+enum TileCfg {
+    TILE_AUTO = 0,
+    TILE_256x256 = 1,     // 2x4 waves of 128x64, 2 stages x 128 B, 128 KB
+    TILE_256x128 = 2,     // 4x2 waves of  64x64, 3 stages x 128 B, 144 KB
+    TILE_128x128 = 3,     // 2x2 waves of  64x64, 4 stages x 128 B, 128 KB
+    TILE_128x256 = 4,     // 2x4 waves of  64x64, 3 stages x 128 B, 144 KB
+    TILE_64x128 = 5,      // 2x2 waves of  32x64, 4 stages x 128 B,  96 KB
+    TILE_32x128 = 6,      // 1x2 waves of  32x64, 4 stages x 128 B,  80 KB
+    TILE_256x256_W4 = 7,  // 2x2 waves of 128x128, 4 stages x 64 B, 128 KB
+    TILE_256x256_S4 = 8,  // 2x4 waves of 128x64, 4 stages x 64 B, 128 KB
+};
+
+static int g_forced_tile = TILE_AUTO;
+static int forced_tile() { return __atomic_load_n(&g_forced_tile, __ATOMIC_RELAXED); }
+
+bool set_gemm_tile(int tile) {
+    if (tile < TILE_AUTO || tile > TILE_256x256_S4) return false;
+    __atomic_store_n(&g_forced_tile, tile, __ATOMIC_RELAXED);
+    return true;
+}
+
+template <bool F32, int EPI>
+static hipError_t launch_tile(int tile, GemmArgs g, hipStream_t s) {
+    switch (tile) {
+        case TILE_256x256: return launch_cfg<256, 256, 2, 4, 2, 8, F32, EPI>(g, s);
+        case TILE_256x128: return launch_cfg<256, 128, 4, 2, 3, 8, F32, EPI>(g, s);
+        case TILE_128x128: return launch_cfg<128, 128, 2, 2, 4, 8, F32, EPI>(g, s);
+        case TILE_128x256: return launch_cfg<128, 256, 2, 4, 3, 8, F32, EPI>(g, s);
+        case TILE_64x128: return launch_cfg<64, 128, 2, 2, 4, 8, F32, EPI>(g, s);
+        case TILE_256x256_W4: return launch_cfg<256, 256, 2, 2, 4, 4, F32, EPI>(g, s);
+        case TILE_256x256_S4: return launch_cfg<256, 256, 2, 4, 4, 4, F32, EPI>(g, s);
+        default: return launch_cfg<32, 128, 1, 2, 4, 8, F32, EPI>(g, s);
+    }
+}
+
 // Tile shape by tokens per expert: many rows per expert favour large tiles
 // (fewer LDS and L2 bytes per flop); few rows favour short tiles (no MFMA
-// work on padding rows).
+// work on padding rows, more workgroups to spread a weight stream over).
 template <bool F32, int EPI>
 static hipError_t launch_by_shape(GemmArgs g, hipStream_t s) {
+    const int f = forced_tile();
+    if (f > 0) return launch_tile<F32, EPI>(f, g, s);
     const int64_t per_expert = g.T / (g.E > 0 ? g.E : 1);
-    if (!F32 && per_expert >= 768) return launch_cfg<256, 256, 2, 2, F32, EPI>(g, s);
-    if (per_expert >= 96) return launch_cfg<128, 128, 2, 2, F32, EPI>(g, s);
-    return launch_cfg<32, 128, 1, 2, F32, EPI>(g, s);
+    if (per_expert >= 768) return launch_tile<F32, EPI>(TILE_256x256, g, s);
+    if (per_expert >= 96) return launch_tile<F32, EPI>(TILE_128x128, g, s);
+    return launch_tile<F32, EPI>(TILE_32x128, g, s);
 }
 
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s) {

@@ -36,6 +36,7 @@ hipError_t launch_move_rows(int64_t nrows, int64_t row_bytes, const void* src, c
 hipError_t launch_pack(readme_dtype dt, int64_t E, int64_t d, int64_t I, const void* wg,
                        const void* wu, const void* wd, void* packed, hipStream_t s);
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s);
+bool set_gemm_tile(int tile);
 hipError_t launch_rms_to_bf16(int64_t T, int64_t d, const float* x, const int32_t* offsets, int E,
                               float eps, uint16_t* xn, hipStream_t s);
 

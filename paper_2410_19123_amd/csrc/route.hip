@@ -18,19 +18,24 @@ template <int W>
 struct Chunk;
 template <>
 struct Chunk<8> {  // 8 bf16
-    __device__ static void load(const void* base, int64_t idx, float* v) {
-        const uint4 q = reinterpret_cast<const uint4*>(base)[idx];
+    __device__ static void unpack(const uint4 q, float* v) {
         v[0] = bf16_lo(q.x); v[1] = bf16_hi(q.x);
         v[2] = bf16_lo(q.y); v[3] = bf16_hi(q.y);
         v[4] = bf16_lo(q.z); v[5] = bf16_hi(q.z);
         v[6] = bf16_lo(q.w); v[7] = bf16_hi(q.w);
     }
+    __device__ static void load(const void* base, int64_t idx, float* v) {
+        unpack(reinterpret_cast<const uint4*>(base)[idx], v);
+    }
 };
 template <>
 struct Chunk<4> {  // 4 fp32
+    __device__ static void unpack(const uint4 q, float* v) {
+        v[0] = __uint_as_float(q.x); v[1] = __uint_as_float(q.y);
+        v[2] = __uint_as_float(q.z); v[3] = __uint_as_float(q.w);
+    }
     __device__ static void load(const void* base, int64_t idx, float* v) {
-        const float4 q = reinterpret_cast<const float4*>(base)[idx];
-        v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+        unpack(reinterpret_cast<const uint4*>(base)[idx], v);
     }
 };
 
@@ -112,6 +117,104 @@ __global__ __launch_bounds__(256) void k_route(int64_t T, int64_t d, int E,
     }
 }
 
+// Register-resident variant for rows of at most 64*CPL chunks: the lane's
+// chunks of its R token rows are loaded once, up front; the router rows are
+// then streamed expert by expert with the next expert's chunks in flight
+// while the current one is summed.  Same summation order as k_route.
+template <int R, int CPL, int W>
+__global__ __launch_bounds__(256) void k_route_reg(int64_t T, int64_t d, int E,
+                                                   const void* __restrict__ x,
+                                                   const void* __restrict__ wr,
+                                                   const float* __restrict__ bias,
+                                                   int32_t* __restrict__ ids,
+                                                   float* __restrict__ logits) {
+    const int lane = threadIdx.x & 63;
+    const int64_t t0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * R;
+    if (t0 >= T) return;
+    const int nchunks = (int)(d / W);
+    const uint4* xq = reinterpret_cast<const uint4*>(x);
+    const uint4* wq = reinterpret_cast<const uint4*>(wr);
+
+    uint4 xr[R][CPL];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int64_t row = (t0 + r < T ? t0 + r : T - 1) * nchunks;
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            const int c = lane + 64 * j;
+            xr[r][j] = c < nchunks ? xq[row + c] : make_uint4(0, 0, 0, 0);
+        }
+    }
+    auto load_w = [&](uint4* wb, int e) {
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            const int c = lane + 64 * j;
+            wb[j] = c < nchunks ? wq[(int64_t)e * nchunks + c] : make_uint4(0, 0, 0, 0);
+        }
+    };
+
+    float best[R];
+    int bid[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) { best[r] = 0.0f; bid[r] = 0; }
+
+    // Logit of expert e from router chunks wb, then the running argmax.
+    auto expert = [&](const uint4* wb, int e) {
+        float acc[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) acc[r] = 0.0f;
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            if (lane + 64 * j >= nchunks) break;
+            float wv[W];
+            Chunk<W>::unpack(wb[j], wv);
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                float xv[W];
+                Chunk<W>::unpack(xr[r][j], xv);
+#pragma unroll
+                for (int q = 0; q < W; ++q) acc[r] = __builtin_fmaf(xv[q], wv[q], acc[r]);
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            float v = acc[r];
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) {
+                const float o = __shfl_down(v, off, 64);
+                v = v + o;
+            }
+            float logit = __shfl(v, 0, 64);
+            if (bias) logit = logit + bias[e];
+            if (logits && lane == 0 && t0 + r < T) logits[(t0 + r) * E + e] = logit;
+            if (e == 0) {
+                best[r] = logit;
+                bid[r] = 0;
+            } else if (logit > best[r]) {
+                best[r] = logit;
+                bid[r] = e;
+            }
+        }
+    };
+
+    // Two named buffers (not an array indexed by e & 1, which would go to
+    // scratch): the next expert's row is in flight while this one is summed.
+    uint4 wa[CPL], wb[CPL];
+    load_w(wa, 0);
+    for (int e = 0; e < E; e += 2) {
+        if (e + 1 < E) load_w(wb, e + 1);
+        expert(wa, e);
+        if (e + 1 >= E) break;
+        if (e + 2 < E) load_w(wa, e + 2);
+        expert(wb, e + 1);
+    }
+    if (lane == 0) {
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            if (t0 + r < T) ids[t0 + r] = bid[r];
+    }
+}
+
 template <int R, int W>
 static hipError_t launch_route_r(int64_t T, int64_t d, int E, const void* x, const void* w,
                                  const float* bias, int32_t* ids, float* logits,
@@ -126,9 +229,35 @@ static hipError_t launch_route_r(int64_t T, int64_t d, int E, const void* x, con
     return hipGetLastError();
 }
 
+template <int R, int W>
+static hipError_t launch_route_reg(int cpl, int64_t T, int64_t d, int E, const void* x,
+                                   const void* w, const float* bias, int32_t* ids, float* logits,
+                                   hipStream_t s) {
+    const dim3 grid((unsigned)ceil_div(T, 4 * R)), block(256);
+    switch (cpl) {
+        case 1: k_route_reg<R, 1, W><<<grid, block, 0, s>>>(T, d, E, x, w, bias, ids, logits); break;
+        case 2: k_route_reg<R, 2, W><<<grid, block, 0, s>>>(T, d, E, x, w, bias, ids, logits); break;
+        case 4: k_route_reg<R, 4, W><<<grid, block, 0, s>>>(T, d, E, x, w, bias, ids, logits); break;
+        case 8: k_route_reg<R, 8, W><<<grid, block, 0, s>>>(T, d, E, x, w, bias, ids, logits); break;
+        default: k_route_reg<R, 16, W><<<grid, block, 0, s>>>(T, d, E, x, w, bias, ids, logits); break;
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_route(readme_dtype dt, int64_t T, int64_t d, int E, const void* x,
                         const void* w, const float* bias, int32_t* ids, float* logits,
                         hipStream_t s) {
+    // Rows of up to 1024 chunks (8192 bf16 / 4096 fp32) stay in registers.
+    const int64_t nchunks = d / (dt == README_BF16 ? 8 : 4);
+    if (nchunks <= 64 * 16) {
+        int cpl = 1;
+        while (64 * cpl < nchunks) cpl *= 2;
+        if (dt == README_BF16)
+            return T >= 8192 ? launch_route_reg<2, 8>(cpl, T, d, E, x, w, bias, ids, logits, s)
+                             : launch_route_reg<1, 8>(cpl, T, d, E, x, w, bias, ids, logits, s);
+        return T >= 8192 ? launch_route_reg<2, 4>(cpl, T, d, E, x, w, bias, ids, logits, s)
+                         : launch_route_reg<1, 4>(cpl, T, d, E, x, w, bias, ids, logits, s);
+    }
     // Few tokens: one token per wave spreads the work over the chip; many
     // tokens: four per wave so that one router-row load serves four tokens.
     const bool many = T >= 8192;

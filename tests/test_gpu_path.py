@@ -269,3 +269,24 @@ def test_decode_stack_teacher_forced(L, oracle_mod):
     y = L.readme_ungroup(xa, inv)
     torch.cuda.synchronize()
     assert (U.from_dev(y) == U.from_dev(xa)[U.from_dev(inv)]).all()
+
+
+# ------------------------------------------------------ every tile config
+@pytest.mark.parametrize("tile", [1, 2, 3, 4, 5, 6])
+def test_every_gemm_tile_matches_oracle(L, oracle_mod, tile):
+    """Each workgroup tile of the grouped GEMM, on ragged blocks (empty,
+    single-row, tile +- 1 and multi-tile experts) in bf16 and fp32."""
+    _say("tile", tile)
+    L.readme_set_gemm_tile(tile)
+    try:
+        for dtype, d, I, counts in [("bf16", 256, 200, [0, 1, 255, 257, 33, 520]),
+                                    ("f32", 128, 96, [3, 0, 129, 64])]:
+            E, T = len(counts), sum(counts)
+            w = wl.Workload("t", T=T, d=d, E=E, I=I, dtype=dtype)
+            x = wl.make_x(w, 10 + tile)
+            wg, wu, wd = wl.make_experts(w, 10 + tile)
+            offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+            y, _ = _run_ffn(L, x, offsets, wg, wu, wd, E, I)
+            U.close(y, oracle_mod.moe_ffn(x, offsets, wg, wu, wd), f"tile {tile} {dtype}")
+    finally:
+        L.readme_set_gemm_tile(0)
