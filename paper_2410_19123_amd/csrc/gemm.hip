@@ -312,13 +312,15 @@ enum TileCfg {
     TILE_32x128 = 6,      // 1x2 waves of  32x64, 4 stages x 128 B,  80 KB
     TILE_256x256_W4 = 7,  // 2x2 waves of 128x128, 4 stages x 64 B, 128 KB
     TILE_256x256_S4 = 8,  // 2x4 waves of 128x64, 4 stages x 64 B, 128 KB
+    TILE_128x256_2WG = 9, // 2x4 waves of  64x64, 3 stages x 64 B,  72 KB (2 per CU)
+    TILE_64x256_2WG = 10, // 1x4 waves of  64x64, 4 stages x 64 B,  80 KB (2 per CU)
 };
 
 static int g_forced_tile = TILE_AUTO;
 static int forced_tile() { return __atomic_load_n(&g_forced_tile, __ATOMIC_RELAXED); }
 
 bool set_gemm_tile(int tile) {
-    if (tile < TILE_AUTO || tile > TILE_256x256_S4) return false;
+    if (tile < TILE_AUTO || tile > TILE_64x256_2WG) return false;
     __atomic_store_n(&g_forced_tile, tile, __ATOMIC_RELAXED);
     return true;
 }
@@ -333,20 +335,26 @@ static hipError_t launch_tile(int tile, GemmArgs g, hipStream_t s) {
         case TILE_64x128: return launch_cfg<64, 128, 2, 2, 4, 8, F32, EPI>(g, s);
         case TILE_256x256_W4: return launch_cfg<256, 256, 2, 2, 4, 4, F32, EPI>(g, s);
         case TILE_256x256_S4: return launch_cfg<256, 256, 2, 4, 4, 4, F32, EPI>(g, s);
+        case TILE_128x256_2WG: return launch_cfg<128, 256, 2, 4, 3, 4, F32, EPI>(g, s);
+        case TILE_64x256_2WG: return launch_cfg<64, 256, 1, 4, 4, 4, F32, EPI>(g, s);
         default: return launch_cfg<32, 128, 1, 2, 4, 8, F32, EPI>(g, s);
     }
 }
 
-// Tile shape by tokens per expert: many rows per expert favour large tiles
-// (fewer LDS and L2 bytes per flop); few rows favour short tiles (no MFMA
-// work on padding rows, more workgroups to spread a weight stream over).
+// Tile shape by tokens per expert (the host knows T and E, not the split):
+// many rows per expert favour large tiles (fewer LDS and L2 bytes per
+// flop); few rows favour short tiles (no MFMA work on padding rows, more
+// workgroups to spread a weight stream over).  The down projection (N = d)
+// has more N tiles than gate/up at these shapes, so it switches to the
+// large tile earlier.  Thresholds come from tile sweeps on MI355X.
 template <bool F32, int EPI>
 static hipError_t launch_by_shape(GemmArgs g, hipStream_t s) {
     const int f = forced_tile();
     if (f > 0) return launch_tile<F32, EPI>(f, g, s);
     const int64_t per_expert = g.T / (g.E > 0 ? g.E : 1);
-    if (per_expert >= 768) return launch_tile<F32, EPI>(TILE_256x256, g, s);
-    if (per_expert >= 96) return launch_tile<F32, EPI>(TILE_128x128, g, s);
+    const int64_t big = EPI == EPI_GATE_UP_SILU ? 768 : 192;
+    if (per_expert >= big) return launch_tile<F32, EPI>(TILE_256x256, g, s);
+    if (per_expert >= 96) return launch_tile<F32, EPI>(TILE_128x256, g, s);
     return launch_tile<F32, EPI>(TILE_32x128, g, s);
 }
 
