@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target length of the oracle's timed sample")
+    ap.add_argument("--unfused", action="store_true",
+                    help="separate row gather / ungroup calls instead of the row moves "
+                         "fused into the two GEMMs")
     ap.add_argument("--gemm-tile", type=int, default=0,
                     help="force a grouped-GEMM tile configuration (0 = automatic)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -164,17 +167,40 @@ class Path:
         self._ok(self.lib.readme_ungroup(0, w.T, w.d, P(self.xres), P(self.inv),
                                          P(self.yres), self.stream), "ungroup")
 
-    def calls(self, k):
-        """(name, call) of one step, in path order; k picks the weight copy."""
+    def group_only(self):
+        P, w = self.P, self.w
+        self._ok(self.lib.readme_group_by_expert(
+            w.T, w.E, P(self.ids), P(self.counts), P(self.offsets), P(self.perm), P(self.inv),
+            self.dt, w.d, None, None, self.stream), "group")
+
+    def gate_up_gather(self, k):
+        P, w = self.P, self.w
+        self._ok(self.lib.readme_moe_gate_up_gather(
+            self.dt, w.T, w.d, w.E, w.I, P(self.x), P(self.perm), P(self.offsets),
+            P(self.packed[k]), P(self.h), self.stream), "gate_up_gather")
+
+    def down_scatter(self, k):
+        P, w = self.P, self.w
+        self._ok(self.lib.readme_moe_down_scatter(
+            self.dt, w.T, w.d, w.E, w.I, P(self.h), P(self.perm), P(self.offsets),
+            P(self.packed[k]), P(self.y), self.stream), "down_scatter")
+
+    def calls(self, k, fused=True):
+        """(name, call) of one step, in path order; k picks the weight copy.
+        fused: the row gather and the ungroup ride in the two GEMMs."""
         if self.w.layers > 1:
             return [("route", self.route), ("group", self.group_resid),
                     ("stack", self.stack), ("ungroup", self.ungroup_resid)]
+        if fused:
+            return [("route", self.route), ("group", self.group_only),
+                    ("gate_up", lambda: self.gate_up_gather(k)),
+                    ("down", lambda: self.down_scatter(k))]
         return [("route", self.route), ("group", self.group),
                 ("gate_up", lambda: self.gate_up(k)), ("down", lambda: self.down(k)),
                 ("ungroup", self.ungroup)]
 
 
-def algorithmic(w: wl.Workload, counts: np.ndarray) -> dict:
+def algorithmic(w: wl.Workload, counts: np.ndarray, fused: bool = False) -> dict:
     """Algorithmic bytes and flops per launch of each kernel (unpadded I,
     weights of active experts only, each byte counted once)."""
     s = w.elem_bytes
@@ -195,7 +221,7 @@ def algorithmic(w: wl.Workload, counts: np.ndarray) -> dict:
         }
     return {
         "route": dict(bytes=T * d * s + E * d * s + 4 * T, flops=2.0 * T * d * E),
-        "group": dict(bytes=4 * T + 8 * T + 8 * E + 2 * n * d * s, flops=0.0),
+        "group": dict(bytes=4 * T + 8 * T + 8 * E + (0 if fused else 2 * n * d * s), flops=0.0),
         "gate_up": dict(bytes=active * 2 * I * d * s + n * d * s + n * I * s,
                         flops=4.0 * n * d * I),
         "down": dict(bytes=active * I * d * s + n * I * s + n * d * s, flops=2.0 * n * d * I),
@@ -255,13 +281,14 @@ def main():
     K, W = args.steps, args.warmup
     ncopy = len(path.packed)
 
-    names = [n for n, _ in path.calls(0)]
+    fused = not args.unfused
+    names = [n for n, _ in path.calls(0, fused)]
     ev = {n: [] for n in names}
 
     def step(i, timed):
         k = i % ncopy
         marks = []
-        for n, fn in path.calls(k):
+        for n, fn in path.calls(k, fused):
             if timed:
                 a = torch.cuda.Event(enable_timing=True)
                 a.record()
@@ -289,7 +316,7 @@ def main():
     ms_per_step = gpu_ms / K
 
     counts = path.counts.cpu().numpy()
-    work = algorithmic(w, counts)
+    work = algorithmic(w, counts, fused)
     kern_us = {n: (1e3 * float(np.mean([a.elapsed_time(b) for a, b in ev[n]])) if ev[n] else None)
                for n in names}
 
@@ -316,7 +343,8 @@ def main():
             roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": pk, "unit": "TFLOP/s",
                     "frac": round(ach / pk, 4), "traffic": None}
         roof["kernel"] = ("readme_moe_ffn_stack (all layers)" if layers > 1
-                          else "k_grouped_gemm (gate/up + SiLU*mul)")
+                          else "k_grouped_gemm (gate/up + SiLU*mul"
+                          + (", rows gathered through perm)" if fused else ")"))
         roof["launch_us"] = round(kern_us[dom], 2)
         roof["algorithmic_bytes"] = int(wk["bytes"])
         roof["algorithmic_flops"] = wk["flops"]
@@ -336,6 +364,7 @@ def main():
         "data": "synthetic (seeded N(0,1) tokens, N(0,0.02) weights)",
         "config": {"workload": w.name, "T": w.T, "d": w.d, "E": w.E, "I": w.I,
                    "gemm_tile": args.gemm_tile,
+                   "row_moves": "separate" if args.unfused or layers > 1 else "fused into GEMMs",
                    "layers": layers, "weight_copies_rotated": ncopy,
                    "tokens_per_expert": counts.tolist()},
         "ffn_tflops": round(ffn_flops / (ms_per_step * 1e-3) / 1e12, 2),

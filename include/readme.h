@@ -18,6 +18,8 @@
  *                             row gather into expert-contiguous order
  *     readme_moe_ffn          every expert's SwiGLU FFN on its token block
  *                             (= readme_moe_gate_up then readme_moe_down)
+ *     readme_moe_ffn_fused    gather + FFN + ungroup, row moves fused into
+ *                             the two GEMMs
  *     readme_ungroup          rows back to token order
  *     readme_moe_ffn_stack    L stacked pre-norm residual layers in grouped
  *                             order (routing and grouping done once)
@@ -201,6 +203,47 @@ readme_status readme_moe_down(readme_dtype dt, int64_t T, int64_t d,
                               int32_t E, int64_t I, const void *h,
                               const int32_t *offsets, const void *packed,
                               void *y_grouped, void *stream);
+
+/*
+ * readme_moe_ffn_fused -- readme_group_by_expert's row gather, readme_moe_ffn
+ * and readme_ungroup in two launches: the gate/up GEMM reads its activation
+ * rows straight from token order through perm, and the down GEMM writes
+ * each output row straight to its token's row through perm.
+ *   x [T][d] dt (token order), perm [T] and offsets [E+1] int32 from
+ *   readme_group_by_expert (called without a gather), packed as for
+ *   readme_moe_ffn, y [T][d] dt out (token order), workspace as for
+ *   readme_moe_ffn.
+ * Results equal readme_moe_ffn followed by readme_ungroup bit for bit
+ * (same tiles, same summation order), except that rows of unrouted tokens
+ * (ids outside [0, E)) are not written here.  Map entries outside [0, T)
+ * are clamped on reads and skipped on writes.
+ */
+readme_status readme_moe_ffn_fused(readme_dtype dt, int64_t T, int64_t d,
+                                   int32_t E, int64_t I, const void *x,
+                                   const int32_t *perm, const int32_t *offsets,
+                                   const void *packed, void *y,
+                                   void *workspace, size_t workspace_bytes,
+                                   void *stream);
+
+/*
+ * The two halves of readme_moe_ffn_fused:
+ *   readme_moe_gate_up_gather: h as readme_moe_gate_up, activation row of
+ *     grouped row j taken from x[perm[j]] (x in token order);
+ *   readme_moe_down_scatter:   readme_moe_down with output row j written
+ *     to y[perm[j]] (y in token order).
+ */
+readme_status readme_moe_gate_up_gather(readme_dtype dt, int64_t T, int64_t d,
+                                        int32_t E, int64_t I, const void *x,
+                                        const int32_t *perm,
+                                        const int32_t *offsets,
+                                        const void *packed, void *h,
+                                        void *stream);
+readme_status readme_moe_down_scatter(readme_dtype dt, int64_t T, int64_t d,
+                                      int32_t E, int64_t I, const void *h,
+                                      const int32_t *perm,
+                                      const int32_t *offsets,
+                                      const void *packed, void *y,
+                                      void *stream);
 
 /*
  * readme_ungroup -- rows back to token order: y[t] = y_grouped[inv_perm[t]],

@@ -38,6 +38,10 @@ SIGNATURES = {
     "readme_moe_ffn_workspace_bytes": (_SZ, [_I32, _I64, _I64]),
     "readme_moe_ffn": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _SZ, _P]),
     "readme_moe_gate_up": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P]),
+    "readme_moe_ffn_fused": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _P, _SZ,
+                                    _P]),
+    "readme_moe_gate_up_gather": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _P]),
+    "readme_moe_down_scatter": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _P]),
     "readme_moe_down": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P]),
     "readme_ungroup": (_I32, [_I32, _I64, _I64, _P, _P, _P, _P]),
     "readme_moe_ffn_stack_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
@@ -184,6 +188,42 @@ def readme_moe_ffn(x_grouped, offsets, packed, E, I, y_grouped=None, workspace=N
           _p(y_grouped), _p(workspace), workspace.numel() * workspace.element_size(),
           _stream(x_grouped.device))
     return y_grouped
+
+
+def readme_moe_ffn_fused(x, perm, offsets, packed, E, I, y=None, workspace=None):
+    """Gather + expert FFN + ungroup with the row moves inside the GEMMs;
+    returns y in token order (rows of unrouted tokens are not written)."""
+    T, d = x.shape
+    if y is None:
+        y = torch.empty_like(x)
+    ws = readme_moe_ffn_workspace_bytes(x.dtype, T, I)
+    if workspace is None:
+        workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=x.device)
+    _dev(x, perm, offsets, packed, y, workspace)
+    _call("readme_moe_ffn_fused", _dt(x), T, d, E, I, _p(x), _p(perm), _p(offsets), _p(packed),
+          _p(y), _p(workspace), workspace.numel() * workspace.element_size(),
+          _stream(x.device))
+    return y
+
+
+def readme_moe_gate_up_gather(x, perm, offsets, packed, E, I, h=None):
+    """readme_moe_gate_up reading activation rows through perm (token order x)."""
+    T, d = x.shape
+    if h is None:
+        h = torch.empty(T, readme_padded_intermediate(I), dtype=x.dtype, device=x.device)
+    _dev(x, perm, offsets, packed, h)
+    _call("readme_moe_gate_up_gather", _dt(x), T, d, E, I, _p(x), _p(perm), _p(offsets),
+          _p(packed), _p(h), _stream(x.device))
+    return h
+
+
+def readme_moe_down_scatter(h, perm, offsets, packed, E, I, d, y):
+    """readme_moe_down writing output rows through perm (token order y)."""
+    T = h.shape[0]
+    _dev(h, perm, offsets, packed, y)
+    _call("readme_moe_down_scatter", _dt(h), T, d, E, I, _p(h), _p(perm), _p(offsets),
+          _p(packed), _p(y), _stream(h.device))
+    return y
 
 
 def readme_moe_gate_up(x_grouped, offsets, packed, E, I, h=None):

@@ -180,6 +180,50 @@ readme_status readme_moe_ffn(readme_dtype dt, int64_t T, int64_t d, int32_t E, i
     return readme_moe_down(dt, T, d, E, I, workspace, offsets, packed, y_grouped, stream);
 }
 
+readme_status readme_moe_gate_up_gather(readme_dtype dt, int64_t T, int64_t d, int32_t E,
+                                        int64_t I, const void* x, const int32_t* perm,
+                                        const int32_t* offsets, const void* packed, void* h,
+                                        void* stream) {
+    readme_status st = check_ffn_shape(dt, T, d, E, I);
+    if (st != README_OK) return st;
+    if (T == 0) return README_OK;
+    if (!x || !perm || !offsets || !packed || !h) return README_ERR_ARG;
+    if (!a16(x) || !a16(packed)) return README_ERR_ARG;
+    GemmArgs g = gate_up_args(dt, T, d, E, I, x, offsets, packed, h);
+    g.a_rows = perm;  // grouped row j reads token row perm[j]
+    return hip_status(
+        launch_grouped_gemm(dt == README_F32, EPI_GATE_UP_SILU, g, as_stream(stream)));
+}
+
+readme_status readme_moe_down_scatter(readme_dtype dt, int64_t T, int64_t d, int32_t E,
+                                      int64_t I, const void* h, const int32_t* perm,
+                                      const int32_t* offsets, const void* packed, void* y,
+                                      void* stream) {
+    readme_status st = check_ffn_shape(dt, T, d, E, I);
+    if (st != README_OK) return st;
+    if (T == 0) return README_OK;
+    if (!h || !perm || !offsets || !packed || !y) return README_ERR_ARG;
+    if (!a16(h) || !a16(packed)) return README_ERR_ARG;
+    GemmArgs g = down_args(dt, T, d, E, I, h, offsets, packed, y);
+    g.c_rows = perm;  // grouped row j lands in token row perm[j]
+    return hip_status(launch_grouped_gemm(dt == README_F32, EPI_STORE, g, as_stream(stream)));
+}
+
+readme_status readme_moe_ffn_fused(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I,
+                                   const void* x, const int32_t* perm, const int32_t* offsets,
+                                   const void* packed, void* y, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+    readme_status st = check_ffn_shape(dt, T, d, E, I);
+    if (st != README_OK) return st;
+    if (T == 0) return README_OK;
+    if (!x || !perm || !offsets || !packed || !y || !workspace) return README_ERR_ARG;
+    if (!a16(y) || !a16(workspace)) return README_ERR_ARG;
+    if (workspace_bytes < readme_moe_ffn_workspace_bytes(dt, T, I)) return README_ERR_WORKSPACE;
+    st = readme_moe_gate_up_gather(dt, T, d, E, I, x, perm, offsets, packed, workspace, stream);
+    if (st != README_OK) return st;
+    return readme_moe_down_scatter(dt, T, d, E, I, workspace, perm, offsets, packed, y, stream);
+}
+
 readme_status readme_ungroup(readme_dtype dt, int64_t T, int64_t d, const void* y_grouped,
                              const int32_t* inv_perm, void* y, void* stream) {
     if (!dtype_ok(dt) || T < 0 || d <= 0) return README_ERR_ARG;

@@ -100,10 +100,14 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     static_assert(NSTAGE >= 2 && LPS * (NSTAGE - 2) < 64, "stages");
 
     __shared__ u32x4 lds[NSTAGE * STAGE];
+    __shared__ int32_t crow[BM];  // output row of each tile row (row map)
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    // The wave index is uniform across a wave; readfirstlane tells the
+    // compiler so, which keeps every wave-level quantity (tile offsets, LDS
+    // bases of the DMA, loop conditions) in scalar registers.
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WGN, wn = wave % WGN;
 
     // Linear tile index, remapped so that each XCD gets a contiguous run.
@@ -114,7 +118,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     // Find (expert, M tile, N tile) of L: experts in order, each expert's
     // tiles in groups of GROUP_M M tiles, N tiles outer, M tiles inner.
     int e = -1, n_tile = 0;
-    int64_t m0 = 0;
+    int64_t m0 = 0, m_end = 0;
     int rows = 0;
     {
         int64_t acc = 0, prev = 0;
@@ -135,6 +139,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
                 const int mt = grp * GROUP_M + (within - n_tile * gm);
                 e = ee;
                 m0 = s + (int64_t)mt * BM;
+                m_end = en;
                 rows = (int)((en - m0) < BM ? (en - m0) : BM);
                 break;
             }
@@ -146,9 +151,10 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
 
     // This lane's DMA sources.  Instruction i of this wave fills tile rows
     // r = RPI*(wave + NW*i) + lane/CPR, slot lane%CPR, which holds the
-    // logical chunk swz(lane%CPR, r) (an XOR: its own inverse).  Rows are
-    // clamped in bounds; rows past the expert's block are fetched and never
-    // stored.
+    // logical chunk swz(lane%CPR, r) (an XOR: its own inverse).  Rows past
+    // the expert's block are clamped to its last row (fetched, never
+    // stored); with a row map the A row comes from a_rows[row], which is a
+    // valid row for every row inside the block.
     const int rsub = lane / CPR;
     const char* Ab = reinterpret_cast<const char*>(g.A);
     const char* Bb = reinterpret_cast<const char*>(g.B) + (int64_t)e * g.b_expert_stride * ESZ;
@@ -158,7 +164,11 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     for (int i = 0; i < A_INS; ++i) {
         const int r = RPI * (wave + NW * i) + rsub;
         int64_t row = m0 + r;
-        row = row < g.T ? row : g.T - 1;
+        row = row < m_end ? row : m_end - 1;
+        if (g.a_rows) {
+            row = g.a_rows[row];
+            row = (row >= 0 && row < g.T) ? row : 0;  // a corrupt map stays in bounds
+        }
         a_src[i] = Ab + row * g.lda * ESZ + swz<CPR>(lane % CPR, r) * 16;
     }
 #pragma unroll
@@ -179,6 +189,17 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
         for (int i = 0; i < B_INS; ++i)
             dma16(b_src[i] + koff, base + (BM + RPI * (wave + NW * i)) * CPR);
     };
+
+    // Output rows of this tile, staged once: the epilogue then needs no
+    // dependent global load (the first K-step's barrier orders this store
+    // before every read).
+    if (g.c_rows) {
+        for (int r = tid; r < BM; r += NW * 64) {
+            int64_t row = m0 + r;
+            row = row < m_end ? row : m_end - 1;
+            crow[r] = g.c_rows[row];
+        }
+    }
 
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -222,9 +243,6 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
             const int cb = kk & 1;
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
-                // 32-row sub-tiles wholly past the expert's last row do no
-                // MFMA work (wave-uniform branch; their rows are never stored).
-                if (wm * WM + i * 32 >= rows) continue;
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
                     if constexpr (F32) {
@@ -252,7 +270,8 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
         for (int r = 0; r < 16; ++r) {
             const int rt = wm * WM + i * 32 + 8 * (r >> 2) + 4 * fhalf + (r & 3);
             if (rt >= rows) continue;
-            const int64_t grow = m0 + rt;
+            const int64_t grow = g.c_rows ? (int64_t)crow[rt] : m0 + rt;
+            if (grow < 0 || grow >= g.T) continue;  // a corrupt map writes nothing
             if constexpr (EPI == EPI_GATE_UP_SILU) {
 #pragma unroll
                 for (int j = 0; j < TN; j += 2) {

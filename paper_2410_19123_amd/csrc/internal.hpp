@@ -23,6 +23,10 @@ struct GemmArgs {
     int64_t T;
     void* C;                  // [T][ldc] output
     int64_t ldc;              // elements
+    // Optional row maps (fused row moves): A row j is read from A row
+    // a_rows[j]; output row j is written to C row c_rows[j].  NULL = identity.
+    const int32_t* a_rows;
+    const int32_t* c_rows;
     int n_tiles, m_tiles_max; // filled by the launcher
 };
 

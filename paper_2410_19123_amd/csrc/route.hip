@@ -229,6 +229,150 @@ static hipError_t launch_route_r(int64_t T, int64_t d, int E, const void* x, con
     return hipGetLastError();
 }
 
+// LDS-resident variant: the whole router matrix (E*d elements, at most
+// LDS_BYTES) is staged in LDS once per workgroup; each of the 8 waves then
+// walks R-token groups of the workgroup's TB tokens with the token rows in
+// registers, reading router chunks from LDS (consecutive lanes read
+// consecutive 16 bytes: conflict-free).  Same summation order as k_route.
+template <int R, int CPL, int W, int LDS_BYTES, int EB>
+__global__ __launch_bounds__(512) void k_route_lds(int64_t T, int64_t d, int E, int tb,
+                                                   const void* __restrict__ x,
+                                                   const void* __restrict__ wr,
+                                                   const float* __restrict__ bias,
+                                                   int32_t* __restrict__ ids,
+                                                   float* __restrict__ logits) {
+    __shared__ uint4 wl[LDS_BYTES / 16];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int nchunks = (int)(d / W);
+    const uint4* xq = reinterpret_cast<const uint4*>(x);
+    {
+        const uint4* wq = reinterpret_cast<const uint4*>(wr);
+        const int n = E * nchunks;
+        for (int i = threadIdx.x; i < n; i += 512) wl[i] = wq[i];
+    }
+    __syncthreads();
+
+    const int64_t tb0 = (int64_t)blockIdx.x * tb;
+    for (int g = wave; g * R < tb; g += 8) {
+        const int64_t t0 = tb0 + (int64_t)g * R;
+        if (t0 >= T) break;
+        uint4 xr[R][CPL];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int64_t row = (t0 + r < T ? t0 + r : T - 1) * nchunks;
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) {
+                const int c = lane + 64 * j;
+                xr[r][j] = c < nchunks ? xq[row + c] : make_uint4(0, 0, 0, 0);
+            }
+        }
+        float best[R];
+        int bid[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) { best[r] = 0.0f; bid[r] = 0; }
+        // Experts in blocks of EB: all R x EB partial sums are formed first,
+        // then folded together, so the cross-lane shuffles of different
+        // (token, expert) pairs overlap instead of running one chain at a
+        // time.  Each pair's own order is the canonical one.
+        for (int e0 = 0; e0 < E; e0 += EB) {
+            float acc[R][EB];
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int b = 0; b < EB; ++b) acc[r][b] = 0.0f;
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) {
+                const int c = lane + 64 * j;
+                if (c >= nchunks) break;
+                float xv[R][W];
+#pragma unroll
+                for (int r = 0; r < R; ++r) Chunk<W>::unpack(xr[r][j], xv[r]);
+#pragma unroll
+                for (int b = 0; b < EB; ++b) {
+                    if (e0 + b >= E) break;
+                    float wv[W];
+                    Chunk<W>::unpack(wl[(e0 + b) * nchunks + c], wv);
+#pragma unroll
+                    for (int r = 0; r < R; ++r)
+#pragma unroll
+                        for (int q = 0; q < W; ++q)
+                            acc[r][b] = __builtin_fmaf(xv[r][q], wv[q], acc[r][b]);
+                }
+            }
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1)
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+#pragma unroll
+                    for (int b = 0; b < EB; ++b) {
+                        const float o = __shfl_down(acc[r][b], off, 64);
+                        acc[r][b] = acc[r][b] + o;
+                    }
+#pragma unroll
+            for (int b = 0; b < EB; ++b) {
+                const int e = e0 + b;
+                if (e >= E) break;
+#pragma unroll
+                for (int r = 0; r < R; ++r) {
+                    float logit = __shfl(acc[r][b], 0, 64);
+                    if (bias) logit = logit + bias[e];
+                    if (logits && lane == 0 && t0 + r < T) logits[(t0 + r) * E + e] = logit;
+                    if (e == 0) {
+                        best[r] = logit;
+                        bid[r] = 0;
+                    } else if (logit > best[r]) {
+                        best[r] = logit;
+                        bid[r] = e;
+                    }
+                }
+            }
+        }
+        if (lane == 0) {
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                if (t0 + r < T) ids[t0 + r] = bid[r];
+        }
+    }
+}
+
+template <int R, int CPL, int W, int LDS_BYTES>
+static hipError_t launch_route_lds_r(int64_t T, int64_t d, int E, const void* x, const void* w,
+                                     const float* bias, int32_t* ids, float* logits,
+                                     hipStream_t s) {
+    // Tokens per workgroup: enough workgroups to fill the chip, and enough
+    // tokens per workgroup to amortise staging the router matrix.
+    int64_t tb = ceil_div(T, 256);
+    tb = tb < 8 ? 8 : (tb > 128 ? 128 : tb);
+    tb = round_up(tb, R);
+    const dim3 grid((unsigned)ceil_div(T, tb)), block(512);
+    // Expert block: up to 16 partial sums per token, fewer when the token
+    // rows already take many registers (two waves per SIMD, no spills).
+    constexpr int EBMAX = R * CPL >= 16 ? 8 : 16;
+    if (E <= 4)
+        k_route_lds<R, CPL, W, LDS_BYTES, 4><<<grid, block, 0, s>>>(T, d, E, (int)tb, x, w, bias, ids, logits);
+    else if (E <= 8)
+        k_route_lds<R, CPL, W, LDS_BYTES, 8><<<grid, block, 0, s>>>(T, d, E, (int)tb, x, w, bias, ids, logits);
+    else
+        k_route_lds<R, CPL, W, LDS_BYTES, EBMAX><<<grid, block, 0, s>>>(T, d, E, (int)tb, x, w, bias, ids, logits);
+    return hipGetLastError();
+}
+
+// R tokens per wave group: as many as the token rows' registers allow with
+// two waves per SIMD (no spills).
+template <int W, int LDS_BYTES>
+static hipError_t launch_route_lds(int cpl, int64_t T, int64_t d, int E, const void* x,
+                                   const void* w, const float* bias, int32_t* ids, float* logits,
+                                   hipStream_t s) {
+    switch (cpl) {
+        case 1: return launch_route_lds_r<4, 1, W, LDS_BYTES>(T, d, E, x, w, bias, ids, logits, s);
+        case 2: return launch_route_lds_r<4, 2, W, LDS_BYTES>(T, d, E, x, w, bias, ids, logits, s);
+        case 4: return launch_route_lds_r<4, 4, W, LDS_BYTES>(T, d, E, x, w, bias, ids, logits, s);
+        case 8: return launch_route_lds_r<2, 8, W, LDS_BYTES>(T, d, E, x, w, bias, ids, logits, s);
+        default: return launch_route_lds_r<1, 16, W, LDS_BYTES>(T, d, E, x, w, bias, ids, logits, s);
+    }
+}
+
 template <int R, int W>
 static hipError_t launch_route_reg(int cpl, int64_t T, int64_t d, int E, const void* x,
                                    const void* w, const float* bias, int32_t* ids, float* logits,
@@ -252,6 +396,18 @@ hipError_t launch_route(readme_dtype dt, int64_t T, int64_t d, int E, const void
     if (nchunks <= 64 * 16) {
         int cpl = 1;
         while (64 * cpl < nchunks) cpl *= 2;
+        // Router matrix in LDS when it fits (64 KB, or 128 KB for many tokens).
+        const int64_t wbytes = (int64_t)E * d * (dt == README_BF16 ? 2 : 4);
+        if (wbytes <= 65536) {
+            if (dt == README_BF16)
+                return launch_route_lds<8, 65536>(cpl, T, d, E, x, w, bias, ids, logits, s);
+            return launch_route_lds<4, 65536>(cpl, T, d, E, x, w, bias, ids, logits, s);
+        }
+        if (wbytes <= 131072 && T >= 8192) {
+            if (dt == README_BF16)
+                return launch_route_lds<8, 131072>(cpl, T, d, E, x, w, bias, ids, logits, s);
+            return launch_route_lds<4, 131072>(cpl, T, d, E, x, w, bias, ids, logits, s);
+        }
         if (dt == README_BF16)
             return T >= 8192 ? launch_route_reg<2, 8>(cpl, T, d, E, x, w, bias, ids, logits, s)
                              : launch_route_reg<1, 8>(cpl, T, d, E, x, w, bias, ids, logits, s);

@@ -290,3 +290,43 @@ def test_every_gemm_tile_matches_oracle(L, oracle_mod, tile):
             U.close(y, oracle_mod.moe_ffn(x, offsets, wg, wu, wd), f"tile {tile} {dtype}")
     finally:
         L.readme_set_gemm_tile(0)
+
+
+# ------------------------------------------------------------ fused moves
+@pytest.mark.parametrize("name", ["tiny_f32", "llama7b_layer", "prefill_skew16",
+                                  "wide_requests"])
+def test_fused_row_moves_equal_unfused(L, name):
+    """Gather in the gate/up loads and scatter in the down epilogue give the
+    same bits as the separate gather, FFN and ungroup calls."""
+    w = wl.WORKLOADS[name]
+    _say("fused", name)
+    x = U.to_dev(wl.make_x(w))
+    wr, b = wl.make_router(w)
+    if w.router:
+        ids, _ = L.readme_route(x, U.to_dev(wr), None if b is None else U.to_dev(b))
+    else:
+        ids = U.to_dev(wl.make_request_ids(w))
+    counts, offs, perm, inv, xg = L.readme_group_by_expert(ids, w.E, x=x)
+    packed = L.readme_pack_experts(*U.weights_to_dev(*wl.make_experts(w)))
+    y_ref = L.readme_ungroup(L.readme_moe_ffn(xg, offs, packed, w.E, w.I), inv)
+    y = L.readme_moe_ffn_fused(x, perm, offs, packed, w.E, w.I)
+    torch.cuda.synchronize()
+    assert (U.from_dev(y) == U.from_dev(y_ref)).all()
+
+
+def test_fused_leaves_unrouted_rows_untouched(L):
+    T, d, E, I = 300, 128, 5, 96
+    w = wl.Workload("t", T=T, d=d, E=E, I=I, dtype="bf16")
+    x = U.to_dev(wl.make_x(w, 12))
+    rng = np.random.default_rng(12)
+    ids_h = rng.integers(-1, E + 1, size=T).astype(np.int32)
+    counts, offs, perm, inv, xg = L.readme_group_by_expert(U.to_dev(ids_h), E, x=x)
+    packed = L.readme_pack_experts(*U.weights_to_dev(*wl.make_experts(w, 12)))
+    y = torch.full((T, d), 7.0, dtype=torch.bfloat16, device=U.dev())
+    L.readme_moe_ffn_fused(x, perm, offs, packed, E, I, y=y)
+    y_ref = L.readme_ungroup(L.readme_moe_ffn(xg, offs, packed, E, I), inv)
+    torch.cuda.synchronize()
+    yh, rh = U.from_dev(y), U.from_dev(y_ref)
+    routed = (ids_h >= 0) & (ids_h < E)
+    assert (yh[routed] == rh[routed]).all()
+    assert (wl.bf16_bits_to_f32(yh[~routed]) == 7.0).all()
