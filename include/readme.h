@@ -158,7 +158,8 @@ int64_t readme_padded_intermediate(int64_t I);
  * process-wide, for tuning and for testing every configuration.
  *   0 = automatic (by tokens per expert, the default)
  *   1 = 256x256, 2 = 256x128, 3 = 128x128, 4 = 128x256, 5 = 64x128,
- *   6 = 32x128  (rows of tokens x columns of outputs)
+ *   6 = 32x128, 7 = 32x64 (deep pipeline), 8 = 32x128 (deep pipeline)
+ *   (rows of tokens x columns of outputs)
  * Results do not depend on the tile beyond fp32 summation order.  Returns
  * README_ERR_ARG for any other value.  Not synchronised with calls in
  * flight on other host threads.

@@ -32,14 +32,8 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-# Per-source extra flags.  The grouped GEMM asks LLVM's AMDGPU machine
-# scheduler for its iterative ILP strategy, which keeps the next k-slice's
-# LDS fragment reads in flight under the current slice's MFMAs (the default
-# strategy shortens register live ranges by loading each fragment just
-# before its first use, which stalls a one-wave-per-SIMD kernel).
-EXTRA = {
-    "gemm.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"],
-}
+# Per-source extra flags (none at present).
+EXTRA: dict = {}
 
 
 def _compile(src: str) -> str:

@@ -9,6 +9,8 @@
 //                     alternate), output h = silu(g) * u in registers;
 //   EPI_STORE         B_e = W_down, output y;
 //   EPI_RESID_ADD     B_e = W_down, fp32 residual += y (stacked layers).
+// Optional row maps gather A rows (a_rows) and scatter output rows (c_rows),
+// which lets the row moves around the FFN ride inside the two GEMMs.
 //
 // Tiling.  A workgroup owns a BM x BN output tile of one expert; each of its
 // WGM x WGN waves owns a (BM/WGM) x (BN/WGN) sub-tile made of 32x32 MFMA
@@ -17,17 +19,20 @@
 // operands use the same k order inside a fragment, so the product is exact
 // whatever order the unit sums in).
 //
-// Data movement.  A K-step moves CPR 16-byte chunks of every A and B row
-// (CPR = 8: 128 bytes = 64 bf16 / 32 fp32; CPR = 4: 64 bytes) straight from
-// global memory into LDS with global_load_lds_dwordx4 (no VGPR staging).
-// One such wave instruction fills 1 KB of LDS = 1024 / (16 CPR) rows.  A
-// 16-byte fragment read serves 16 lanes = 16 consecutive rows per LDS cycle
-// over 64 four-byte banks, and a row covers 4 CPR of them, so the 16 rows
-// must land on 16 distinct 16-byte bank groups: chunk c of row r is stored
-// in slot c ^ ((r / (8 / CPR)) % CPR) -- for CPR = 8, rows alternate bank
-// halves and the XOR spreads each parity class; for CPR = 4, rows cycle
-// through four quarters and the XOR spreads each class.  The swizzle is
-// applied on the global side by choosing which chunk each lane fetches.
+// Data movement.  A K-step moves 128 bytes of every A and B row (64 bf16 /
+// 32 fp32) from global memory straight into LDS with global_load_lds_dwordx4
+// (no VGPR staging); one wave instruction fills 1 KB = 8 rows.  In LDS,
+// 16-byte chunk c of tile row r sits in slot r*8 + (c ^ ((r >> 1) & 7)): a
+// fragment read serves 16 lanes = 16 consecutive rows per LDS cycle over 64
+// four-byte banks, a 128-byte row covers half of them and rows alternate
+// halves, so each parity class needs 8 distinct slots -- the XOR gives that
+// and the reads are bank-conflict free.
+//   A (activations, row-major): each lane fetches the chunk its slot holds,
+//     i.e. the swizzle is applied on the global side.
+//   B (packed weights): stored already in blocks of 32 rows x 128 bytes in
+//     the LDS slot order (see pack.hip), so each DMA instruction copies one
+//     contiguous KB and a workgroup streams each weight row group as one
+//     sequential run (4 KB per K-step), which keeps DRAM pages open.
 // NSTAGE K-steps are in flight: at step kt the workgroup waits for stage kt
 // (s_waitcnt vmcnt counts this wave's later stages), meets at one barrier,
 // refills the buffer freed by step kt-1 with step kt+NSTAGE-1, then runs
@@ -72,30 +77,26 @@ __device__ __forceinline__ void block_barrier() {
     asm volatile("" ::: "memory");
 }
 
+// LDS slot of logical 16-byte chunk c of tile row r (an XOR: its own inverse).
+__device__ __forceinline__ int swz(int c, int r) { return c ^ ((r >> 1) & 7); }
+
 constexpr int GROUP_M = 4;
+constexpr int CPR = 8;  // 16-byte chunks per row per K-step (128 bytes)
 
-// LDS slot of logical chunk c of tile row r (see the bank analysis above).
-template <int CPR>
-__device__ __forceinline__ int swz(int c, int r) {
-    return c ^ ((r / (8 / CPR)) % CPR);
-}
-
-template <int BM, int BN, int WGM, int WGN, int NSTAGE, int CPR, bool F32, int EPI>
+template <int BM, int BN, int WGM, int WGN, int NSTAGE, bool F32, int EPI>
 __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     constexpr int NW = WGM * WGN;
     constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int TM = WM / 32, TN = WN / 32;
-    constexpr int RPI = 64 / CPR;          // tile rows per DMA instruction
     constexpr int EPC = F32 ? 4 : 8;       // elements per chunk
     constexpr int BK = CPR * EPC;          // K elements per step
     constexpr int ESZ = F32 ? 4 : 2;
-    constexpr int A_INS = BM / RPI / NW;   // DMA instructions per wave per stage
-    constexpr int B_INS = BN / RPI / NW;
+    constexpr int A_INS = BM / 8 / NW;     // DMA instructions per wave per stage
+    constexpr int B_INS = BN / 8 / NW;
     constexpr int LPS = A_INS + B_INS;
     constexpr int STAGE = (BM + BN) * CPR; // u32x4 slots per stage
     static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile");
-    static_assert(CPR == 4 || CPR == 8, "chunks per row");
-    static_assert(A_INS * RPI * NW == BM && B_INS * RPI * NW == BN, "DMA split");
+    static_assert(A_INS * 8 * NW == BM && B_INS * 8 * NW == BN, "DMA split");
     static_assert(EPI != EPI_GATE_UP_SILU || WN % 64 == 0, "gate/up pairs");
     static_assert(NSTAGE >= 2 && LPS * (NSTAGE - 2) < 64, "stages");
 
@@ -149,45 +150,50 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     if (e < 0) return;
     const int64_t n0 = (int64_t)n_tile * BN;
 
-    // This lane's DMA sources.  Instruction i of this wave fills tile rows
-    // r = RPI*(wave + NW*i) + lane/CPR, slot lane%CPR, which holds the
-    // logical chunk swz(lane%CPR, r) (an XOR: its own inverse).  Rows past
-    // the expert's block are clamped to its last row (fetched, never
-    // stored); with a row map the A row comes from a_rows[row], which is a
-    // valid row for every row inside the block.
-    const int rsub = lane / CPR;
+    // A sources.  Instruction i of this wave fills tile rows 8*(wave+NW*i)
+    // .. +7: lane -> row +lane/8, slot lane%8, which holds logical chunk
+    // swz(lane%8, r).  Rows past the expert's block are clamped to its last
+    // row (fetched, never stored); with a row map the A row comes from
+    // a_rows[row], a valid token row for every row inside the block.
+    const int rsub = lane >> 3;
     const char* Ab = reinterpret_cast<const char*>(g.A);
-    const char* Bb = reinterpret_cast<const char*>(g.B) + (int64_t)e * g.b_expert_stride * ESZ;
     const char* a_src[A_INS];
-    const char* b_src[B_INS];
 #pragma unroll
     for (int i = 0; i < A_INS; ++i) {
-        const int r = RPI * (wave + NW * i) + rsub;
+        const int r = 8 * (wave + NW * i) + rsub;
         int64_t row = m0 + r;
         row = row < m_end ? row : m_end - 1;
         if (g.a_rows) {
             row = g.a_rows[row];
             row = (row >= 0 && row < g.T) ? row : 0;  // a corrupt map stays in bounds
         }
-        a_src[i] = Ab + row * g.lda * ESZ + swz<CPR>(lane % CPR, r) * 16;
+        a_src[i] = Ab + row * g.lda * ESZ + swz(lane & 7, r) * 16;
     }
+    // B sources: blocked weights, (32-row group, K step) blocks of 4 KB.
+    // Instruction i copies tile rows 8*(wave+NW*i) .. +7 = one contiguous KB
+    // of their group's block; N tiles past the last group reuse it (their
+    // columns are never stored).
+    const int64_t ksteps = g.K / BK;
+    const char* Bb = reinterpret_cast<const char*>(g.B) + (int64_t)e * g.b_expert_stride * ESZ;
+    const char* b_src[B_INS];
 #pragma unroll
     for (int i = 0; i < B_INS; ++i) {
-        const int r = RPI * (wave + NW * i) + rsub;
-        int64_t row = n0 + r;
-        row = row < g.N ? row : g.N - 1;
-        b_src[i] = Bb + row * g.ldb * ESZ + swz<CPR>(lane % CPR, r) * 16;
+        const int r = 8 * (wave + NW * i);
+        int64_t grp = (n0 + r) >> 5;
+        const int64_t last = (g.N >> 5) - 1;
+        grp = grp < last ? grp : last;
+        b_src[i] = Bb + (grp * ksteps * 32 + (r & 31)) * 128 + lane * 16;
     }
 
     auto issue = [&](int stage, int kt) {
         u32x4* base = lds + stage * STAGE;
-        const int64_t koff = (int64_t)kt * (CPR * 16);
+        const int64_t aoff = (int64_t)kt * 128;
+        const int64_t boff = (int64_t)kt * 4096;
 #pragma unroll
-        for (int i = 0; i < A_INS; ++i)
-            dma16(a_src[i] + koff, base + RPI * (wave + NW * i) * CPR);
+        for (int i = 0; i < A_INS; ++i) dma16(a_src[i] + aoff, base + 8 * (wave + NW * i) * CPR);
 #pragma unroll
         for (int i = 0; i < B_INS; ++i)
-            dma16(b_src[i] + koff, base + (BM + RPI * (wave + NW * i)) * CPR);
+            dma16(b_src[i] + boff, base + (BM + 8 * (wave + NW * i)) * CPR);
     };
 
     // Output rows of this tile, staged once: the epilogue then needs no
@@ -209,7 +215,27 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    const int nk = (int)(g.K / BK);
+    // Residual epilogue: the residual values this wave will update are read
+    // now, ahead of the K loop, so the epilogue does not wait on them (each
+    // element belongs to exactly one workgroup, so nothing else writes it).
+    if constexpr (EPI == EPI_RESID_ADD) {
+        const float* res = reinterpret_cast<const float*>(g.C);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int rt = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                const int64_t grow = m0 + (rt < rows ? rt : 0);
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    int64_t c = n0 + wn * WN + j * 32 + (lane & 31);
+                    c = c < g.N ? c : g.N - 1;
+                    acc[i][j][r] = res[grow * g.ldc + c];
+                }
+            }
+    }
+
+    const int nk = (int)ksteps;
 #pragma unroll
     for (int s = 0; s < NSTAGE - 1; ++s)
         if (s < nk) issue(s, s);
@@ -230,7 +256,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
         const u32x4* S = lds + (kt % NSTAGE) * STAGE;
         u32x4 af[2][TM], bfr[2][TN];
         auto frag = [&](int buf, int kk) {
-            const int ch = swz<CPR>(2 * kk + fhalf, frow);
+            const int ch = swz(2 * kk + fhalf, frow);
 #pragma unroll
             for (int i = 0; i < TM; ++i) af[buf][i] = S[a_row0 + i * 32 * CPR + ch];
 #pragma unroll
@@ -291,8 +317,8 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
                     const int64_t c = n0 + wn * WN + j * 32 + col;
                     const float v = acc[i][j][r];
                     if constexpr (EPI == EPI_RESID_ADD) {
-                        float* y = reinterpret_cast<float*>(g.C) + grow * g.ldc + c;
-                        *y = *y + v;
+                        // acc started from the residual value: store the sum.
+                        reinterpret_cast<float*>(g.C)[grow * g.ldc + c] = v;
                     } else if constexpr (F32) {
                         reinterpret_cast<float*>(g.C)[grow * g.ldc + c] = v;
                     } else {
@@ -304,7 +330,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     }
 }
 
-template <int BM, int BN, int WGM, int WGN, int NSTAGE, int CPR, bool F32, int EPI>
+template <int BM, int BN, int WGM, int WGN, int NSTAGE, bool F32, int EPI>
 static hipError_t launch_cfg(GemmArgs g, hipStream_t s) {
     g.n_tiles = (int)ceil_div(g.N, BN);
     int64_t mt = (g.T + (int64_t)g.E * (BM - 1)) / BM;
@@ -313,33 +339,31 @@ static hipError_t launch_cfg(GemmArgs g, hipStream_t s) {
     const int64_t blocks = round_up((int64_t)g.n_tiles * g.m_tiles_max, 8);
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    k_grouped_gemm<BM, BN, WGM, WGN, NSTAGE, CPR, F32, EPI>
+    k_grouped_gemm<BM, BN, WGM, WGN, NSTAGE, F32, EPI>
         <<<dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, s>>>(g);
     return hipGetLastError();
 }
 
-// Tile configurations: workgroup tile, wave grid (wave tile), K-stages in
-// flight x bytes per row per stage, LDS.  readme_set_gemm_tile() forces one
-// process-wide.
+// Tile configurations: workgroup tile, wave grid (wave tile), K-steps in
+// flight, LDS.  readme_set_gemm_tile() forces one process-wide.
 enum TileCfg {
     TILE_AUTO = 0,
-    TILE_256x256 = 1,     // 2x4 waves of 128x64, 2 stages x 128 B, 128 KB
-    TILE_256x128 = 2,     // 4x2 waves of  64x64, 3 stages x 128 B, 144 KB
-    TILE_128x128 = 3,     // 2x2 waves of  64x64, 4 stages x 128 B, 128 KB
-    TILE_128x256 = 4,     // 2x4 waves of  64x64, 3 stages x 128 B, 144 KB
-    TILE_64x128 = 5,      // 2x2 waves of  32x64, 4 stages x 128 B,  96 KB
-    TILE_32x128 = 6,      // 1x2 waves of  32x64, 4 stages x 128 B,  80 KB
-    TILE_256x256_W4 = 7,  // 2x2 waves of 128x128, 4 stages x 64 B, 128 KB
-    TILE_256x256_S4 = 8,  // 2x4 waves of 128x64, 4 stages x 64 B, 128 KB
-    TILE_128x256_2WG = 9, // 2x4 waves of  64x64, 3 stages x 64 B,  72 KB (2 per CU)
-    TILE_64x256_2WG = 10, // 1x4 waves of  64x64, 4 stages x 64 B,  80 KB (2 per CU)
+    TILE_256x256 = 1,  // 2x4 waves of 128x64, 2 stages, 128 KB
+    TILE_256x128 = 2,  // 4x2 waves of  64x64, 3 stages, 144 KB
+    TILE_128x128 = 3,  // 2x2 waves of  64x64, 4 stages, 128 KB
+    TILE_128x256 = 4,  // 2x4 waves of  64x64, 3 stages, 144 KB
+    TILE_64x128 = 5,   // 2x2 waves of  32x64, 4 stages,  96 KB
+    TILE_32x128 = 6,   // 1x2 waves of  32x64, 4 stages,  80 KB (few rows per expert)
+    TILE_32x64 = 7,    // 1 wave of 32x64, 6 stages, 72 KB (2 per CU; decode)
+    TILE_32x128_S6 = 8,  // 1x2 waves of 32x64, 6 stages, 120 KB (decode)
+    TILE_LAST = TILE_32x128_S6,
 };
 
 static int g_forced_tile = TILE_AUTO;
 static int forced_tile() { return __atomic_load_n(&g_forced_tile, __ATOMIC_RELAXED); }
 
 bool set_gemm_tile(int tile) {
-    if (tile < TILE_AUTO || tile > TILE_64x256_2WG) return false;
+    if (tile < TILE_AUTO || tile > TILE_LAST) return false;
     __atomic_store_n(&g_forced_tile, tile, __ATOMIC_RELAXED);
     return true;
 }
@@ -347,16 +371,14 @@ bool set_gemm_tile(int tile) {
 template <bool F32, int EPI>
 static hipError_t launch_tile(int tile, GemmArgs g, hipStream_t s) {
     switch (tile) {
-        case TILE_256x256: return launch_cfg<256, 256, 2, 4, 2, 8, F32, EPI>(g, s);
-        case TILE_256x128: return launch_cfg<256, 128, 4, 2, 3, 8, F32, EPI>(g, s);
-        case TILE_128x128: return launch_cfg<128, 128, 2, 2, 4, 8, F32, EPI>(g, s);
-        case TILE_128x256: return launch_cfg<128, 256, 2, 4, 3, 8, F32, EPI>(g, s);
-        case TILE_64x128: return launch_cfg<64, 128, 2, 2, 4, 8, F32, EPI>(g, s);
-        case TILE_256x256_W4: return launch_cfg<256, 256, 2, 2, 4, 4, F32, EPI>(g, s);
-        case TILE_256x256_S4: return launch_cfg<256, 256, 2, 4, 4, 4, F32, EPI>(g, s);
-        case TILE_128x256_2WG: return launch_cfg<128, 256, 2, 4, 3, 4, F32, EPI>(g, s);
-        case TILE_64x256_2WG: return launch_cfg<64, 256, 1, 4, 4, 4, F32, EPI>(g, s);
-        default: return launch_cfg<32, 128, 1, 2, 4, 8, F32, EPI>(g, s);
+        case TILE_256x256: return launch_cfg<256, 256, 2, 4, 2, F32, EPI>(g, s);
+        case TILE_256x128: return launch_cfg<256, 128, 4, 2, 3, F32, EPI>(g, s);
+        case TILE_128x128: return launch_cfg<128, 128, 2, 2, 4, F32, EPI>(g, s);
+        case TILE_128x256: return launch_cfg<128, 256, 2, 4, 3, F32, EPI>(g, s);
+        case TILE_64x128: return launch_cfg<64, 128, 2, 2, 4, F32, EPI>(g, s);
+        case TILE_32x64: return launch_cfg<32, 64, 1, 1, 6, F32, EPI>(g, s);
+        case TILE_32x128_S6: return launch_cfg<32, 128, 1, 2, 6, F32, EPI>(g, s);
+        default: return launch_cfg<32, 128, 1, 2, 4, F32, EPI>(g, s);
     }
 }
 

@@ -1,45 +1,75 @@
 // One-time repack of expert weights into the layout the FFN kernels stream.
 //
-// gate/up block [E][2*Ip][d]: 32-row groups alternate gate (even group g)
-//   and up (odd group g) for intermediate neurons 32*(g/2) .. +31, so a
-//   32-column MFMA tile of gate outputs and the next one of up outputs hold
-//   the same neurons and SiLU(g)*u can be formed in registers.
-// down block [E][d][Ip]: W_down rows with the intermediate axis padded.
+// Logical packed matrices (K-contiguous weight rows, as the GEMM consumes):
+//   gate/up  [E][2*Ip][d]: 32-row groups alternate gate (even group g) and up
+//            (odd group g) for intermediate neurons 32*(g/2) .. +31, so a
+//            32-column MFMA tile of gate outputs and the next one of up
+//            outputs hold the same neurons and SiLU(g)*u forms in registers;
+//   down     [E][d][Ip]: W_down rows, the intermediate axis padded.
 // Neurons i >= I are zero (exact: silu(0) * 0 = 0 and zero columns add 0).
+//
+// Physical layout of each logical [N][K] matrix (N a multiple of 32, K*elt a
+// multiple of 128 bytes): blocks of 32 rows x 128 bytes of K, ordered
+// (row group, K block); inside a block, 16-byte chunk c of row r sits in
+// slot r*8 + (c ^ ((r >> 1) & 7)).  A GEMM workgroup thus streams each row
+// group's weights as one sequential run, 4 KB per K-step (DRAM-friendly),
+// and every 1 KB DMA instruction copies a contiguous KB straight into the
+// bank-conflict-free LDS layout the MFMA fragment reads expect.
 #include "common.hpp"
 #include "internal.hpp"
 
 namespace readme {
 
+// Byte offset of element (n, k) of a blocked [N][K] matrix with `ksteps`
+// 128-byte K blocks per row group, elements of `esz` bytes.
+__device__ __forceinline__ int64_t blocked_offset(int64_t n, int64_t k, int64_t ksteps,
+                                                  int esz) {
+    const int64_t kb = k * esz;               // byte column
+    const int64_t grp = n >> 5, r = n & 31;
+    const int64_t s = kb >> 7, c = (kb >> 4) & 7, inner = kb & 15;
+    const int64_t slot = r * 8 + (c ^ ((r >> 1) & 7));
+    return ((grp * ksteps + s) * 32) * 128 + slot * 16 + inner;
+}
+
+// Gate/up: destination element o of [2*Ip][d] (logical), source gate or up.
 template <typename T>
 __global__ __launch_bounds__(256) void k_pack_gate_up(int64_t E, int64_t d, int64_t I,
                                                       int64_t Ip, const T* __restrict__ wg,
                                                       const T* __restrict__ wu,
-                                                      T* __restrict__ out) {
-    const int64_t total = E * 2 * Ip * d;
+                                                      char* __restrict__ out) {
+    const int64_t per_e = 2 * Ip * d;
+    const int64_t total = E * per_e;
+    const int64_t ksteps = d * (int64_t)sizeof(T) / 128;
     for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total;
          o += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t k = o % d;
-        const int64_t p = (o / d) % (2 * Ip);
-        const int64_t e = o / (d * 2 * Ip);
+        const int64_t e = o / per_e;
+        const int64_t rem = o - e * per_e;
+        const int64_t p = rem / d, k = rem % d;
         const int64_t g = p / 32;
         const int64_t i = (g / 2) * 32 + (p % 32);
         T v = T(0);
         if (i < I) v = ((g & 1) ? wu : wg)[(e * I + i) * d + k];
-        out[o] = v;
+        *reinterpret_cast<T*>(out + e * per_e * (int64_t)sizeof(T) +
+                              blocked_offset(p, k, ksteps, sizeof(T))) = v;
     }
 }
 
+// Down: destination element of [d][Ip] (logical) from W_down [E][d][I].
 template <typename T>
 __global__ __launch_bounds__(256) void k_pack_down(int64_t E, int64_t d, int64_t I, int64_t Ip,
                                                    const T* __restrict__ wd,
-                                                   T* __restrict__ out) {
-    const int64_t total = E * d * Ip;
+                                                   char* __restrict__ out) {
+    const int64_t per_e = d * Ip;
+    const int64_t total = E * per_e;
+    const int64_t ksteps = Ip * (int64_t)sizeof(T) / 128;
     for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total;
          o += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t i = o % Ip;
-        const int64_t row = o / Ip;  // e * d + c
-        out[o] = i < I ? wd[row * I + i] : T(0);
+        const int64_t e = o / per_e;
+        const int64_t rem = o - e * per_e;
+        const int64_t c = rem / Ip, i = rem % Ip;
+        const T v = i < I ? wd[(e * d + c) * I + i] : T(0);
+        *reinterpret_cast<T*>(out + e * per_e * (int64_t)sizeof(T) +
+                              blocked_offset(c, i, ksteps, sizeof(T))) = v;
     }
 }
 
@@ -47,8 +77,8 @@ template <typename T>
 static hipError_t pack_t(int64_t E, int64_t d, int64_t I, const void* wg, const void* wu,
                          const void* wd, void* packed, hipStream_t s) {
     const int64_t Ip = padded_I(I);
-    T* gu = reinterpret_cast<T*>(packed);
-    T* dn = gu + E * 2 * Ip * d;
+    char* gu = reinterpret_cast<char*>(packed);
+    char* dn = gu + E * 2 * Ip * d * (int64_t)sizeof(T);
     const unsigned blocks = 4096;
     k_pack_gate_up<T><<<blocks, 256, 0, s>>>(E, d, I, Ip, reinterpret_cast<const T*>(wg),
                                               reinterpret_cast<const T*>(wu), gu);
