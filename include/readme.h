@@ -157,8 +157,12 @@ int64_t readme_padded_intermediate(int64_t I);
  * readme_set_gemm_tile -- choose the workgroup tile of the grouped GEMMs,
  * process-wide, for tuning and for testing every configuration.
  *   0 = automatic (by tokens per expert, the default)
- *   1 = 256x256, 2 = 256x128, 3 = 128x128, 4 = 128x256, 5 = 64x128,
- *   6 = 32x128, 7 = 32x64 (deep pipeline), 8 = 32x128 (deep pipeline)
+ *   both operands staged in LDS:
+ *     1 = 256x256, 2 = 256x128, 3 = 128x128, 4 = 128x256, 5 = 64x128,
+ *     6 = 32x128, 7 = 32x64 (deep pipeline), 8 = 32x128 (deep pipeline),
+ *     9 = 256x256, 10 = 256x128, 11 = 128x256 (four waves, larger wave tiles)
+ *   weights streamed straight into registers (bf16; fp32 runs tile 6):
+ *     12 = 128x256, 13 = 64x256, 14 = 32x256, 15 = 32x128 (deep pipeline)
  *   (rows of tokens x columns of outputs)
  * Results do not depend on the tile beyond fp32 summation order.  Returns
  * README_ERR_ARG for any other value.  Not synchronised with calls in

@@ -10,11 +10,13 @@
 //
 // Physical layout of each logical [N][K] matrix (N a multiple of 32, K*elt a
 // multiple of 128 bytes): blocks of 32 rows x 128 bytes of K, ordered
-// (row group, K block); inside a block, 16-byte chunk c of row r sits in
-// slot r*8 + (c ^ ((r >> 1) & 7)).  A GEMM workgroup thus streams each row
-// group's weights as one sequential run, 4 KB per K-step (DRAM-friendly),
-// and every 1 KB DMA instruction copies a contiguous KB straight into the
-// bank-conflict-free LDS layout the MFMA fragment reads expect.
+// (row group, K block), each block stored as the four matrix-core operand
+// fragments it holds: 16-byte chunk c of row r goes to fragment c/2, lane
+// (c%2)*32 + r, i.e. byte (c/2)*1024 + ((c%2)*32 + r)*16 of the block.  A
+// fragment is then one contiguous KB that a wave loads with one fully
+// coalesced instruction (lane l takes bytes 16*l .. 16*l+15), whether it goes
+// to registers directly or through LDS, and a workgroup streams each row
+// group's weights as one sequential run, 4 KB per K-step.
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -27,8 +29,8 @@ __device__ __forceinline__ int64_t blocked_offset(int64_t n, int64_t k, int64_t 
     const int64_t kb = k * esz;               // byte column
     const int64_t grp = n >> 5, r = n & 31;
     const int64_t s = kb >> 7, c = (kb >> 4) & 7, inner = kb & 15;
-    const int64_t slot = r * 8 + (c ^ ((r >> 1) & 7));
-    return ((grp * ksteps + s) * 32) * 128 + slot * 16 + inner;
+    const int64_t slot = (c >> 1) * 64 + (c & 1) * 32 + r;
+    return (grp * ksteps + s) * 4096 + slot * 16 + inner;
 }
 
 // Gate/up: destination element o of [2*Ip][d] (logical), source gate or up.
