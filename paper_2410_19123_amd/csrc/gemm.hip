@@ -25,8 +25,8 @@ static int tile_by_shape(bool gate_up, const GemmArgs& g) {
     const int64_t per_expert = g.T / (g.E > 0 ? g.E : 1);
     const int64_t big = gate_up ? 768 : 192;
     if (per_expert >= big) return TILE_256x256;
-    if (per_expert >= 96) return TILE_128x256;
-    return TILE_32x128;
+    if (per_expert >= 96) return gate_up ? TILE_BD_128x256 : TILE_128x256;
+    return TILE_BD_32x128;  // fp32 runs TILE_32x128 instead
 }
 
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s) {

@@ -127,38 +127,79 @@ struct TileLoc {
     int64_t m0, m_end;
 };
 
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int u = __shfl_up(v, off, 64);
+        if (lane >= off) v += u;
+    }
+    return v;
+}
+
 // Maps blockIdx.x to (expert, M tile, N tile); false if past the last tile.
-// The linear tile index is remapped so that each XCD gets a contiguous run;
-// tiles are ordered by expert, then in groups of GROUP_M M tiles with the N
-// tile outer and the M tile inner.
+//
+// Tiles are numbered by expert, then in groups of GROUP_M M tiles with the
+// N tile outer and the M tile inner (so neighbouring tiles share activation
+// rows or weight rows).  The grid is launched for an upper bound of the tile
+// count; the true count comes from the device offsets, each wave reading 64
+// experts at a time in parallel.  The dispatcher deals workgroups to the 8
+// XCDs round-robin (XCD = blockIdx % 8); tile numbers are given out so that
+// each XCD receives one contiguous run of ceil(total/8) tiles, which keeps
+// neighbouring tiles in the same L2 and spreads the work evenly over all
+// XCDs whatever the bound's slack.  Block ranges come from offsets clamped
+// to [0, T], so a corrupt offsets array cannot make a tile leave the rows.
 template <int BM>
 __device__ __forceinline__ bool find_tile(const GemmArgs& g, TileLoc& t) {
-    const int nb = gridDim.x;
-    const int bid = blockIdx.x;
-    const int L = (bid & 7) * (nb >> 3) + (bid >> 3);
-    int64_t acc = 0, prev = 0;
+    const int lane = threadIdx.x & 63;
     const int nt_n = g.n_tiles;
-    for (int ee = 0; ee < g.E; ++ee) {
-        int64_t s = g.offsets[ee], en = g.offsets[ee + 1];
-        s = s < prev ? prev : (s > g.T ? g.T : s);
-        en = en < s ? s : (en > g.T ? g.T : en);
-        prev = en;
-        const int mt_e = (int)((en - s + BM - 1) / BM);
-        const int64_t tiles = (int64_t)mt_e * nt_n;
-        if (L < acc + tiles) {
-            const int local = (int)(L - acc);
+    auto expert = [&](int ee, int& s, int& en) {
+        int64_t a = g.offsets[ee], b = g.offsets[ee + 1];
+        a = a < 0 ? 0 : (a > g.T ? g.T : a);
+        b = b < a ? a : (b > g.T ? g.T : b);
+        s = (int)a;
+        en = (int)b;
+        return (int)((b - a + BM - 1) / BM);
+    };
+    int total = 0;
+    for (int c0 = 0; c0 < g.E; c0 += 64) {
+        int s = 0, en = 0, tiles = 0;
+        if (c0 + lane < g.E) tiles = expert(c0 + lane, s, en) * nt_n;
+        total += __shfl(wave_incl_scan(tiles, lane), 63, 64);
+    }
+    total = __builtin_amdgcn_readfirstlane(total);
+    const int bid = blockIdx.x;
+    const int per_xcd = (total + 7) >> 3;
+    const int j = bid >> 3;
+    if (j >= per_xcd) return false;
+    const int L = (bid & 7) * per_xcd + j;
+    if (L >= total) return false;
+    int base = 0;
+    for (int c0 = 0; c0 < g.E; c0 += 64) {
+        int s = 0, en = 0, mt_e = 0;
+        if (c0 + lane < g.E) mt_e = expert(c0 + lane, s, en);
+        const int tiles = mt_e * nt_n;
+        const int incl = wave_incl_scan(tiles, lane) + base;
+        const uint64_t hit = __ballot(c0 + lane < g.E && L < incl);
+        if (hit) {
+            const int src = __builtin_ctzll(hit);
+            const int e_s = __builtin_amdgcn_readfirstlane(__shfl(s, src, 64));
+            const int e_en = __builtin_amdgcn_readfirstlane(__shfl(en, src, 64));
+            const int e_mt = __builtin_amdgcn_readfirstlane(__shfl(mt_e, src, 64));
+            const int e_incl = __builtin_amdgcn_readfirstlane(__shfl(incl, src, 64));
+            const int local = L - (e_incl - e_mt * nt_n);
             const int grp = local / (GROUP_M * nt_n);
-            const int gm = min(GROUP_M, mt_e - grp * GROUP_M);
+            const int gm = min(GROUP_M, e_mt - grp * GROUP_M);
             const int within = local - grp * GROUP_M * nt_n;
             t.n_tile = within / gm;
             const int mt = grp * GROUP_M + (within - t.n_tile * gm);
-            t.e = ee;
-            t.m0 = s + (int64_t)mt * BM;
-            t.m_end = en;
-            t.rows = (int)((en - t.m0) < BM ? (en - t.m0) : BM);
+            t.e = c0 + src;
+            t.m0 = e_s + (int64_t)mt * BM;
+            t.m_end = e_en;
+            t.rows = (int)((e_en - t.m0) < BM ? (e_en - t.m0) : BM);
             return true;
         }
-        acc += tiles;
+        base = __shfl(incl, 63, 64);
     }
     return false;
 }

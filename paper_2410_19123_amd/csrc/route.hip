@@ -9,6 +9,8 @@
 // at once so that one router-row load feeds R tokens; each router row chunk
 // is a coalesced 1 KB wave load.  The path is VALU-bound (fp32 FMA), not
 // MFMA: an MFMA's internal accumulation order is not this order.
+#include <type_traits>
+
 #include "common.hpp"
 #include "internal.hpp"
 
@@ -246,18 +248,9 @@ __global__ __launch_bounds__(512) void k_route_lds(int64_t T, int64_t d, int E, 
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int nchunks = (int)(d / W);
     const uint4* xq = reinterpret_cast<const uint4*>(x);
-    {
-        const uint4* wq = reinterpret_cast<const uint4*>(wr);
-        const int n = E * nchunks;
-        for (int i = threadIdx.x; i < n; i += 512) wl[i] = wq[i];
-    }
-    __syncthreads();
-
     const int64_t tb0 = (int64_t)blockIdx.x * tb;
-    for (int g = wave; g * R < tb; g += 8) {
-        const int64_t t0 = tb0 + (int64_t)g * R;
-        if (t0 >= T) break;
-        uint4 xr[R][CPL];
+    uint4 xr[R][CPL];
+    auto load_x = [&](int64_t t0) {
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int64_t row = (t0 + r < T ? t0 + r : T - 1) * nchunks;
@@ -267,6 +260,39 @@ __global__ __launch_bounds__(512) void k_route_lds(int64_t T, int64_t d, int E, 
                 xr[r][j] = c < nchunks ? xq[row + c] : make_uint4(0, 0, 0, 0);
             }
         }
+    };
+    // The first token group's rows are requested before the router matrix
+    // is staged, so the two memory latencies overlap (when the rows fit in
+    // registers next to the staging buffer).
+    constexpr bool EARLY = R * CPL < 16;
+    if (EARLY && wave * R < tb && tb0 + wave * R < T) load_x(tb0 + wave * R);
+    {
+        // All loads of the staging are issued before the first LDS store.
+        constexpr int PER = LDS_BYTES / 16 / 512;
+        const uint4* wq = reinterpret_cast<const uint4*>(wr);
+        const int n = E * nchunks;
+        constexpr int BATCH = PER < 8 ? PER : 8;
+#pragma unroll
+        for (int k0 = 0; k0 < PER; k0 += BATCH) {
+            uint4 tmp[BATCH];
+#pragma unroll
+            for (int k = 0; k < BATCH; ++k) {
+                const int i = (int)threadIdx.x + 512 * (k0 + k);
+                tmp[k] = i < n ? wq[i] : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int k = 0; k < BATCH; ++k) {
+                const int i = (int)threadIdx.x + 512 * (k0 + k);
+                if (i < n) wl[i] = tmp[k];
+            }
+        }
+    }
+    __syncthreads();
+
+    for (int g = wave; g * R < tb; g += 8) {
+        const int64_t t0 = tb0 + (int64_t)g * R;
+        if (t0 >= T) break;
+        if (!EARLY || g != wave) load_x(t0);
         float best[R];
         int bid[R];
 #pragma unroll
@@ -364,6 +390,16 @@ template <int W, int LDS_BYTES>
 static hipError_t launch_route_lds(int cpl, int64_t T, int64_t d, int E, const void* x,
                                    const void* w, const float* bias, int32_t* ids, float* logits,
                                    hipStream_t s) {
+    // Few tokens per CU: one token per wave keeps all eight waves busy.
+    if (T <= 4096 && cpl <= 16) {
+        switch (cpl) {
+            case 1: return launch_route_lds_r<1, 1, W, LDS_BYTES>(T, d, E, x, w, bias, ids, logits, s);
+            case 2: return launch_route_lds_r<1, 2, W, LDS_BYTES>(T, d, E, x, w, bias, ids, logits, s);
+            case 4: return launch_route_lds_r<1, 4, W, LDS_BYTES>(T, d, E, x, w, bias, ids, logits, s);
+            case 8: return launch_route_lds_r<1, 8, W, LDS_BYTES>(T, d, E, x, w, bias, ids, logits, s);
+            default: break;
+        }
+    }
     switch (cpl) {
         case 1: return launch_route_lds_r<4, 1, W, LDS_BYTES>(T, d, E, x, w, bias, ids, logits, s);
         case 2: return launch_route_lds_r<4, 2, W, LDS_BYTES>(T, d, E, x, w, bias, ids, logits, s);
