@@ -118,13 +118,15 @@ __device__ __forceinline__ void static_for(F&& f) {
     }
 }
 
-constexpr int GROUP_M = 4;
+constexpr int GROUP_M = 8;
 constexpr int CPR = 8;  // 16-byte chunks per row per K-step (128 bytes)
 
 // Position of this workgroup's output tile.
 struct TileLoc {
     int e, n_tile, rows;
     int64_t m0, m_end;
+    int64_t m_start;  // first grouped row of expert e
+    int mt_base;      // M tiles of size BMG (locate_tile) of experts before e
 };
 
 // Inclusive prefix sum over the 64 lanes of a wave.
@@ -137,49 +139,49 @@ __device__ __forceinline__ int wave_incl_scan(int v, int lane) {
     return v;
 }
 
-// Maps blockIdx.x to (expert, M tile, N tile); false if past the last tile.
-//
-// Tiles are numbered by expert, then in groups of GROUP_M M tiles with the
-// N tile outer and the M tile inner (so neighbouring tiles share activation
-// rows or weight rows).  The grid is launched for an upper bound of the tile
-// count; the true count comes from the device offsets, each wave reading 64
-// experts at a time in parallel.  The dispatcher deals workgroups to the 8
-// XCDs round-robin (XCD = blockIdx % 8); tile numbers are given out so that
-// each XCD receives one contiguous run of ceil(total/8) tiles, which keeps
-// neighbouring tiles in the same L2 and spreads the work evenly over all
-// XCDs whatever the bound's slack.  Block ranges come from offsets clamped
-// to [0, T], so a corrupt offsets array cannot make a tile leave the rows.
+// Rows [s, en) of expert ee, offsets clamped to [0, T] (a corrupt offsets
+// array cannot make a tile leave the rows); returns its M tiles of size BM.
 template <int BM>
-__device__ __forceinline__ bool find_tile(const GemmArgs& g, TileLoc& t) {
+__device__ __forceinline__ int expert_rows(const GemmArgs& g, int ee, int& s, int& en) {
+    int64_t a = g.offsets[ee], b = g.offsets[ee + 1];
+    a = a < 0 ? 0 : (a > g.T ? g.T : a);
+    b = b < a ? a : (b > g.T ? g.T : b);
+    s = (int)a;
+    en = (int)b;
+    return (int)((b - a + BM - 1) / BM);
+}
+
+// Number of BM-row tiles over all experts (times g.n_tiles N tiles), read
+// from the device offsets 64 experts at a time; wave-uniform.
+template <int BM>
+__device__ __forceinline__ int count_tiles(const GemmArgs& g) {
     const int lane = threadIdx.x & 63;
-    const int nt_n = g.n_tiles;
-    auto expert = [&](int ee, int& s, int& en) {
-        int64_t a = g.offsets[ee], b = g.offsets[ee + 1];
-        a = a < 0 ? 0 : (a > g.T ? g.T : a);
-        b = b < a ? a : (b > g.T ? g.T : b);
-        s = (int)a;
-        en = (int)b;
-        return (int)((b - a + BM - 1) / BM);
-    };
     int total = 0;
     for (int c0 = 0; c0 < g.E; c0 += 64) {
         int s = 0, en = 0, tiles = 0;
-        if (c0 + lane < g.E) tiles = expert(c0 + lane, s, en) * nt_n;
+        if (c0 + lane < g.E) tiles = expert_rows<BM>(g, c0 + lane, s, en) * g.n_tiles;
         total += __shfl(wave_incl_scan(tiles, lane), 63, 64);
     }
-    total = __builtin_amdgcn_readfirstlane(total);
-    const int bid = blockIdx.x;
-    const int per_xcd = (total + 7) >> 3;
-    const int j = bid >> 3;
-    if (j >= per_xcd) return false;
-    const int L = (bid & 7) * per_xcd + j;
-    if (L >= total) return false;
-    int base = 0;
+    return __builtin_amdgcn_readfirstlane(total);
+}
+
+// Tile number L -> (expert, M tile, N tile).  Tiles are numbered by expert,
+// then in groups of GROUP_M M tiles with the N tile outer and the M tile
+// inner (so neighbouring tiles share activation rows or weight rows).  Also
+// returns in t.mt_base the number of BMG-row tiles of the experts before e.
+template <int BM, int BMG>
+__device__ __forceinline__ bool locate_tile(const GemmArgs& g, int L, TileLoc& t) {
+    const int lane = threadIdx.x & 63;
+    const int nt_n = g.n_tiles;
+    int base = 0, gbase = 0;
     for (int c0 = 0; c0 < g.E; c0 += 64) {
-        int s = 0, en = 0, mt_e = 0;
-        if (c0 + lane < g.E) mt_e = expert(c0 + lane, s, en);
-        const int tiles = mt_e * nt_n;
-        const int incl = wave_incl_scan(tiles, lane) + base;
+        int s = 0, en = 0, mt_e = 0, mg_e = 0;
+        if (c0 + lane < g.E) {
+            mt_e = expert_rows<BM>(g, c0 + lane, s, en);
+            mg_e = (en - s + BMG - 1) / BMG;
+        }
+        const int incl = wave_incl_scan(mt_e * nt_n, lane) + base;
+        const int gincl = wave_incl_scan(mg_e, lane) + gbase;
         const uint64_t hit = __ballot(c0 + lane < g.E && L < incl);
         if (hit) {
             const int src = __builtin_ctzll(hit);
@@ -187,6 +189,8 @@ __device__ __forceinline__ bool find_tile(const GemmArgs& g, TileLoc& t) {
             const int e_en = __builtin_amdgcn_readfirstlane(__shfl(en, src, 64));
             const int e_mt = __builtin_amdgcn_readfirstlane(__shfl(mt_e, src, 64));
             const int e_incl = __builtin_amdgcn_readfirstlane(__shfl(incl, src, 64));
+            const int e_gincl = __builtin_amdgcn_readfirstlane(__shfl(gincl, src, 64));
+            const int e_mg = __builtin_amdgcn_readfirstlane(__shfl(mg_e, src, 64));
             const int local = L - (e_incl - e_mt * nt_n);
             const int grp = local / (GROUP_M * nt_n);
             const int gm = min(GROUP_M, e_mt - grp * GROUP_M);
@@ -194,14 +198,35 @@ __device__ __forceinline__ bool find_tile(const GemmArgs& g, TileLoc& t) {
             t.n_tile = within / gm;
             const int mt = grp * GROUP_M + (within - t.n_tile * gm);
             t.e = c0 + src;
+            t.m_start = e_s;
             t.m0 = e_s + (int64_t)mt * BM;
             t.m_end = e_en;
             t.rows = (int)((e_en - t.m0) < BM ? (e_en - t.m0) : BM);
+            t.mt_base = e_gincl - e_mg;
             return true;
         }
         base = __shfl(incl, 63, 64);
+        gbase = __shfl(gincl, 63, 64);
     }
     return false;
+}
+
+// Maps blockIdx.x to its tile; false if past the last tile.  The grid is
+// launched for an upper bound of the tile count.  The dispatcher deals
+// workgroups to the 8 XCDs round-robin (XCD = blockIdx % 8); tile numbers are
+// given out so that each XCD receives one contiguous run of ceil(total/8)
+// tiles, which keeps neighbouring tiles in the same L2 and spreads the work
+// evenly over all XCDs whatever the bound's slack.
+template <int BM>
+__device__ __forceinline__ bool find_tile(const GemmArgs& g, TileLoc& t) {
+    const int total = count_tiles<BM>(g);
+    const int bid = blockIdx.x;
+    const int per_xcd = (total + 7) >> 3;
+    const int j = bid >> 3;
+    if (j >= per_xcd) return false;
+    const int L = (bid & 7) * per_xcd + j;
+    if (L >= total) return false;
+    return locate_tile<BM, BM>(g, L, t);
 }
 
 // Residual epilogue (stacked layers, no row maps): the fp32 residual values
@@ -273,22 +298,26 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, const f32x16 (&acc
 
 // Epilogue through LDS.  The accumulator layout gives each lane one column
 // of 16 rows per 32x32 tile, so storing straight from registers means 2- or
-// 4-byte stores scattered over many rows.  Instead the tile is written out
-// in chunks of 32 rows per wave row (WGM*32 rows x all columns): every wave
-// puts its values (converted, SiLU*mul applied) into a row-major LDS chunk,
-// then all threads store the chunk row by row with 16-byte stores, each
-// output row a contiguous run.  Row maps, row bounds and column bounds are
-// applied per 16-byte piece (8 bf16 or 4 fp32 columns; N is a multiple of
-// 64, so a piece is either wholly inside or wholly outside).
-template <int TM, int TN, int WGM, int WGN, bool F32, int EPI>
+// 4-byte stores scattered over many rows.  Instead the tile goes out in as
+// few chunks as the LDS budget allows, CH 32-row sub-tiles per wave row
+// (WGM*32*CH rows x all columns): every wave puts its values (converted,
+// SiLU*mul applied) into a row-major LDS chunk, then all threads store the
+// chunk row by row with 16-byte stores, each output row a contiguous run.
+// Row maps, row bounds and column bounds are applied per 16-byte piece (8
+// bf16 or 4 fp32 columns; N is a multiple of 64, so a piece is either wholly
+// inside or wholly outside).
+template <int TM, int TN, int WGM, int WGN, bool F32, int EPI, int BUDGET>
 struct Epilogue {
     using OT = std::conditional_t<(F32 || EPI == EPI_RESID_ADD), float, uint16_t>;
     static constexpr int BN = WGN * TN * 32;
     static constexpr int OC = EPI == EPI_GATE_UP_SILU ? BN / 2 : BN;  // output columns
     static constexpr int PAD = 16 / (int)sizeof(OT);                 // 16 B row skew
     static constexpr int LDC = OC + PAD;                             // LDS row pitch
-    static constexpr int ROWS = WGM * 32;                            // rows per chunk
-    static constexpr int LDS_BYTES = ROWS * LDC * (int)sizeof(OT);
+    static constexpr int SUB = WGM * 32 * LDC * (int)sizeof(OT);     // bytes per sub-tile row
+    static constexpr int CH = (TM % 4 == 0 && 4 * SUB <= BUDGET) ? 4
+                              : (TM % 2 == 0 && 2 * SUB <= BUDGET) ? 2 : 1;
+    static constexpr int ROWS = WGM * 32 * CH;                       // rows per chunk
+    static constexpr int LDS_BYTES = CH * SUB;
     static constexpr int PER_ROW = OC * (int)sizeof(OT) / 16;        // 16 B pieces per row
 
     __device__ __forceinline__ static OT cvt(float v) {
@@ -306,29 +335,34 @@ struct Epilogue {
         const int64_t oc0 = EPI == EPI_GATE_UP_SILU ? n0 / 2 : n0;  // first output column
         const int64_t n_out = EPI == EPI_GATE_UP_SILU ? g.N / 2 : g.N;
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
+        for (int c = 0; c < TM / CH; ++c) {
             __syncthreads();  // LDS free (K loop or previous chunk done)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int lr = wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                if constexpr (EPI == EPI_GATE_UP_SILU) {
+            for (int ii = 0; ii < CH; ++ii) {
+                const int i = c * CH + ii;
 #pragma unroll
-                    for (int j = 0; j < TN; j += 2) {
-                        const int lc = (wn * TN * 32 + j * 32) / 2 + (lane & 31);
-                        L[lr * LDC + lc] = cvt(silu_f32(acc[i][j][r]) * acc[i][j + 1][r]);
-                    }
-                } else {
+                for (int r = 0; r < 16; ++r) {
+                    const int lr = wm * 32 * CH + ii * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                    if constexpr (EPI == EPI_GATE_UP_SILU) {
 #pragma unroll
-                    for (int j = 0; j < TN; ++j) {
-                        const int lc = wn * TN * 32 + j * 32 + (lane & 31);
-                        L[lr * LDC + lc] = cvt(acc[i][j][r]);
+                        for (int j = 0; j < TN; j += 2) {
+                            const int lc = (wn * TN * 32 + j * 32) / 2 + (lane & 31);
+                            L[lr * LDC + lc] = cvt(silu_f32(acc[i][j][r]) * acc[i][j + 1][r]);
+                        }
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < TN; ++j) {
+                            const int lc = wn * TN * 32 + j * 32 + (lane & 31);
+                            L[lr * LDC + lc] = cvt(acc[i][j][r]);
+                        }
                     }
                 }
             }
             __syncthreads();
             for (int u = tid; u < ROWS * PER_ROW; u += nthreads) {
                 const int lr = u / PER_ROW, pc = u - lr * PER_ROW;
-                const int rt = (lr >> 5) * (TM * 32) + i * 32 + (lr & 31);  // tile row
+                const int w_row = lr / (32 * CH), sub = lr % (32 * CH);
+                const int rt = w_row * (TM * 32) + c * CH * 32 + sub;  // tile row
                 if (rt >= rows) continue;
                 const int64_t grow = g.c_rows ? (int64_t)crow[rt] : m0 + rt;
                 if (grow < 0 || grow >= g.T) continue;  // a corrupt map writes nothing
@@ -358,7 +392,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     static_assert(EPI != EPI_GATE_UP_SILU || WN % 64 == 0, "gate/up pairs");
     static_assert(NSTAGE >= 2 && LPS * (NSTAGE - 2) < 64, "stages");
 
-    using Epi = Epilogue<TM, TN, WGM, WGN, F32, EPI>;
+    using Epi = Epilogue<TM, TN, WGM, WGN, F32, EPI, (NSTAGE * STAGE * 16 > 73728 ? NSTAGE * STAGE * 16 : 73728)>;
     constexpr int LDS_SLOTS = NSTAGE * STAGE > Epi::LDS_BYTES / 16 ? NSTAGE * STAGE : Epi::LDS_BYTES / 16;
     __shared__ u32x4 lds[LDS_SLOTS];
     __shared__ int32_t crow[BM];  // output row of each tile row (row map)
@@ -532,33 +566,63 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
 // Loads past the last K-step re-read K-step nk-1 (never used): every step
 // issues the same loads and the loop needs no conditional loads.
 template <int BM, int NW, int TN, int S, bool F32, int EPI>
-__global__ __launch_bounds__(NW * 64) void k_grouped_gemm_bd(GemmArgs g) {
-    constexpr int TM = BM / 32;
+struct BdTile {
+    static constexpr int TM = BM / 32;
+    static constexpr int STAGE = BM * CPR;  // u32x4 slots per LDS buffer
+    using Epi = Epilogue<TM, TN, 1, NW, F32, EPI, 73728>;
+    static constexpr int LDS_SLOTS =
+        2 * STAGE > Epi::LDS_BYTES / 16 ? 2 * STAGE : Epi::LDS_BYTES / 16;
+
+    // One output tile; lds holds LDS_SLOTS slots, crow BM entries.  Starts
+    // and ends with a barrier, so consecutive tiles may reuse both.
+    __device__ static void run(const GemmArgs& g, const TileLoc& t, u32x4* lds, int32_t* crow) {
     constexpr int WN = TN * 32, BN = NW * WN;
     constexpr int EPC = F32 ? 4 : 8;
     constexpr int BK = CPR * EPC;
     constexpr int ESZ = F32 ? 4 : 2;
     constexpr int A_INS = BM / 8 / NW;    // activation loads per wave per K-step
-    constexpr int STAGE = BM * CPR;       // u32x4 slots per LDS buffer
     static_assert(BM % 32 == 0 && A_INS * 8 * NW == BM, "activation split");
     static_assert(EPI != EPI_GATE_UP_SILU || TN % 2 == 0, "gate/up pairs");
     static_assert(S >= 2, "stages");
 
-    using Epi = Epilogue<TM, TN, 1, NW, F32, EPI>;
-    constexpr int LDS_SLOTS = 2 * STAGE > Epi::LDS_BYTES / 16 ? 2 * STAGE : Epi::LDS_BYTES / 16;
-    __shared__ u32x4 lds[LDS_SLOTS];
-    __shared__ int32_t crow[BM];
-
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    __syncthreads();  // the previous tile's LDS reads are done
 
-    TileLoc t;
-    if (!find_tile<BM>(g, t)) return;
     const int64_t m0 = t.m0, m_end = t.m_end;
     const int rows = t.rows;
     const int64_t n0 = (int64_t)t.n_tile * BN;
     const int64_t col0 = n0 + wave * WN;
+
+    // Weight fragments of this wave: row group (col0/32 + j), clamped to the
+    // last group for columns past N (loaded, never stored).
+    const int64_t ksteps = g.K / BK;
+    const char* Bb = reinterpret_cast<const char*>(g.B) + (int64_t)t.e * g.b_expert_stride * ESZ;
+    const char* b_src[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        int64_t grp = (col0 >> 5) + j;
+        const int64_t last = (g.N >> 5) - 1;
+        grp = grp < last ? grp : last;
+        b_src[j] = Bb + grp * ksteps * 4096 + lane * 16;
+    }
+
+    const int nk = (int)ksteps;
+    u32x4 bq[S][TN][CPR / 2];
+    auto load_b = [&](auto sc, int kt) {
+        constexpr int sl = decltype(sc)::value;
+        kt = kt < nk ? kt : nk - 1;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int q = 0; q < CPR / 2; ++q)
+                bq[sl][j][q] =
+                    *reinterpret_cast<const u32x4*>(b_src[j] + (int64_t)kt * 4096 + q * 1024);
+    };
+    // The weight stream does not depend on the row map: its first K-steps
+    // are requested before the row map is read.
+    static_for<0, S>([&](auto sc) { load_b(sc, decltype(sc)::value); });
 
     // Activation sources: load i of this wave covers tile rows 8*(wave+NW*i)
     // .. +7; lane -> row +lane/8 and LDS slot lane%8, which holds logical
@@ -581,19 +645,7 @@ __global__ __launch_bounds__(NW * 64) void k_grouped_gemm_bd(GemmArgs g) {
         a_src[i] = Ab + row * g.lda * ESZ + swz(lane & 7, r) * 16;
         a_dst[i] = r * CPR + (lane & 7);
     }
-    // Weight fragments of this wave: row group (col0/32 + j), clamped to the
-    // last group for columns past N (loaded, never stored).
-    const int64_t ksteps = g.K / BK;
-    const char* Bb = reinterpret_cast<const char*>(g.B) + (int64_t)t.e * g.b_expert_stride * ESZ;
-    const char* b_src[TN];
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        int64_t grp = (col0 >> 5) + j;
-        const int64_t last = (g.N >> 5) - 1;
-        grp = grp < last ? grp : last;
-        b_src[j] = Bb + grp * ksteps * 4096 + lane * 16;
-    }
-
+    u32x4 aq[S][A_INS];
     if (g.c_rows) {
         for (int r = tid; r < BM; r += NW * 64) {
             int64_t row = m0 + r;
@@ -611,21 +663,16 @@ __global__ __launch_bounds__(NW * 64) void k_grouped_gemm_bd(GemmArgs g) {
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
     if constexpr (EPI == EPI_RESID_ADD) load_residual<TM, TN>(g, acc, 0, col0, rows, m0, lane);
 
-    const int nk = (int)ksteps;
-    u32x4 aq[S][A_INS];
-    u32x4 bq[S][TN][CPR / 2];
-    auto load = [&](auto sc, int kt) {
+    auto load_a = [&](auto sc, int kt) {
         constexpr int sl = decltype(sc)::value;
         kt = kt < nk ? kt : nk - 1;
 #pragma unroll
         for (int i = 0; i < A_INS; ++i)
             aq[sl][i] = *reinterpret_cast<const u32x4*>(a_src[i] + (int64_t)kt * 128);
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-#pragma unroll
-            for (int q = 0; q < CPR / 2; ++q)
-                bq[sl][j][q] =
-                    *reinterpret_cast<const u32x4*>(b_src[j] + (int64_t)kt * 4096 + q * 1024);
+    };
+    auto load = [&](auto sc, int kt) {
+        load_a(sc, kt);
+        load_b(sc, kt);
     };
     auto store_a = [&](auto sc, int buf) {
         constexpr int sl = decltype(sc)::value;
@@ -634,7 +681,7 @@ __global__ __launch_bounds__(NW * 64) void k_grouped_gemm_bd(GemmArgs g) {
     };
 
     // Prologue: K-steps 0 .. S-1 in flight, K-step 0 in LDS buffer 0.
-    static_for<0, S>([&](auto sc) { load(sc, decltype(sc)::value); });
+    static_for<0, S>([&](auto sc) { load_a(sc, decltype(sc)::value); });
     store_a(std::integral_constant<int, 0>{}, 0);
     __syncthreads();
 
@@ -686,6 +733,18 @@ __global__ __launch_bounds__(NW * 64) void k_grouped_gemm_bd(GemmArgs g) {
     });
 
     Epi::run(g, acc, 0, wave, n0, rows, m0, crow, lds, tid, NW * 64);
+    __syncthreads();
+    }
+};
+
+template <int BM, int NW, int TN, int S, bool F32, int EPI>
+__global__ __launch_bounds__(NW * 64) void k_grouped_gemm_bd(GemmArgs g) {
+    using Tile = BdTile<BM, NW, TN, S, F32, EPI>;
+    __shared__ u32x4 lds[Tile::LDS_SLOTS];
+    __shared__ int32_t crow[BM];
+    TileLoc t;
+    if (!find_tile<BM>(g, t)) return;
+    Tile::run(g, t, lds, crow);
 }
 
 template <int BM, int NW, int TN, int SA, bool F32, int EPI>
@@ -737,7 +796,8 @@ enum TileCfg {
     TILE_BD_64x256 = 13,   // 4 waves of 64x64, 4 K-steps
     TILE_BD_32x256 = 14,   // 4 waves of 32x64, 4 K-steps
     TILE_BD_32x128 = 15,   // 2 waves of 32x64, 6 K-steps
-    TILE_LAST = TILE_BD_32x128,
+    TILE_BD_256x256 = 16,  // 4 waves of 256x64, 2 K-steps
+    TILE_LAST = TILE_BD_256x256,
 };
 
 // Launches one tile configuration (instantiated per element type and
@@ -763,6 +823,7 @@ hipError_t launch_tile(int tile, GemmArgs g, hipStream_t s) {
             case TILE_BD_64x256: return launch_bd<64, 4, 2, 4, F32, EPI>(g, s);
             case TILE_BD_32x256: return launch_bd<32, 4, 2, 4, F32, EPI>(g, s);
             case TILE_BD_32x128: return launch_bd<32, 2, 2, 6, F32, EPI>(g, s);
+            case TILE_BD_256x256: return launch_bd<256, 4, 2, 2, F32, EPI>(g, s);
             default: break;
         }
     }

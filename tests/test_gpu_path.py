@@ -272,7 +272,7 @@ def test_decode_stack_teacher_forced(L, oracle_mod):
 
 
 # ------------------------------------------------------ every tile config
-@pytest.mark.parametrize("tile", list(range(1, 16)))
+@pytest.mark.parametrize("tile", list(range(1, 17)))
 def test_every_gemm_tile_matches_oracle(L, oracle_mod, tile):
     """Each workgroup tile of the grouped GEMM, on ragged blocks (empty,
     single-row, tile +- 1 and multi-tile experts) in bf16 and fp32."""
@@ -330,3 +330,4 @@ def test_fused_leaves_unrouted_rows_untouched(L):
     routed = (ids_h >= 0) & (ids_h < E)
     assert (yh[routed] == rh[routed]).all()
     assert (wl.bf16_bits_to_f32(yh[~routed]) == 7.0).all()
+
