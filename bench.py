@@ -200,6 +200,37 @@ class Path:
                 ("ungroup", self.ungroup)]
 
 
+# HBM traffic of the dominant kernel, per launch, from two rocprofv3 --pmc runs of
+# this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each scaled by what
+# the same counter reads for a plain 1 GiB device copy in the same run (--copy-probe:
+# FETCH_SIZE reads 524313 KiB for it, so reads scale by 1.99991; WRITE_SIZE reads
+# exactly 1 GiB, factor 1).  Valid only for the sources the counters were taken
+# with: the entry carries their sha256 and is dropped (traffic null) once any of
+# them changes.
+TRAFFIC_SOURCES = ["csrc/gemm_kernels.hpp", "csrc/gemm.hip", "csrc/gemm_bf16_gate_up.hip",
+                   "csrc/common.hpp", "csrc/internal.hpp", "csrc/pack.hip", "workloads.py"]
+TRAFFIC = {
+    # workload: (sources sha256, read bytes, written bytes) per gate/up launch
+    "llama7b_layer": ("ca767f7524351e2252792cb5d1ca7df1a4569f3961586cbd2e44503b23c4168a",
+                      234279876, 5767168),
+}
+
+
+def traffic_bytes(workload: str):
+    entry = TRAFFIC.get(workload)
+    if entry is None:
+        return None
+    import hashlib
+    root = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2410_19123_amd")
+    h = hashlib.sha256()
+    for rel in TRAFFIC_SOURCES:
+        with open(os.path.join(root, rel), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != entry[0]:
+        return None
+    return entry[1] + entry[2]
+
+
 def algorithmic(w: wl.Workload, counts: np.ndarray, fused: bool = False) -> dict:
     """Algorithmic bytes and flops per launch of each kernel (unpadded I,
     weights of active experts only, each byte counted once)."""
@@ -285,51 +316,65 @@ def main():
     names = [n for n, _ in path.calls(0, fused)]
     ev = {n: [] for n in names}
 
-    def step(i, timed):
+    layers = w.layers
+    dom = "stack" if layers > 1 else "gate_up"
+
+    def step(i, mode):
+        """mode None: no events; "dom": an event pair around the dominant
+        kernel only (the timed region, so events add little to the step);
+        "all": an event before every call (the per-call breakdown pass)."""
         k = i % ncopy
         marks = []
         for n, fn in path.calls(k, fused):
-            if timed:
+            if mode == "all" or (mode == "dom" and n == dom):
                 a = torch.cuda.Event(enable_timing=True)
                 a.record()
                 marks.append((n, a))
             fn()
-        if timed:
+            if mode == "dom" and n == dom:
+                z = torch.cuda.Event(enable_timing=True)
+                z.record()
+                ev_dom.append((marks[-1][1], z))
+        if mode == "all":
             z = torch.cuda.Event(enable_timing=True)
             z.record()
             for j, (n, a) in enumerate(marks):
                 nxt = marks[j + 1][1] if j + 1 < len(marks) else z
                 ev[n].append((a, nxt))
 
+    ev_dom = []
     for i in range(W):
-        step(i, False)
+        step(i, None)
     torch.cuda.synchronize()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     start.record()
     for i in range(K):
-        step(W + i, True)
+        step(W + i, "dom")
     stop.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gpu_ms = start.elapsed_time(stop)
     ms_per_step = gpu_ms / K
+    dom_us = 1e3 * float(np.mean([a.elapsed_time(b) for a, b in ev_dom]))
+    # Per-call breakdown: a separate, shorter pass after the timed region.
+    for i in range(min(K, 20)):
+        step(W + K + i, "all")
+    torch.cuda.synchronize()
 
     counts = path.counts.cpu().numpy()
     work = algorithmic(w, counts, fused)
     kern_us = {n: (1e3 * float(np.mean([a.elapsed_time(b) for a, b in ev[n]])) if ev[n] else None)
                for n in names}
 
-    layers = w.layers
     value = w.T * K / (gpu_ms / 1e3)  # tokens/s through one step
     if layers > 1:
         value = value * layers       # per MoE layer
     ffn_flops = 6.0 * int(counts.sum()) * w.d * w.I * layers
 
-    dom = "stack" if layers > 1 else "gate_up"
     roof = None
-    if kern_us[dom]:
-        t = kern_us[dom] * 1e-6
+    if dom_us:
+        t = dom_us * 1e-6
         wk = work[dom]
         t_hbm = wk["bytes"] / (HBM_GBS * 1e9)
         pk = MFMA_F32_TFLOPS if w.dtype == "f32" else MFMA_BF16_TFLOPS
@@ -345,7 +390,9 @@ def main():
         roof["kernel"] = ("readme_moe_ffn_stack (all layers)" if layers > 1
                           else "k_grouped_gemm (gate/up + SiLU*mul"
                           + (", rows gathered through perm)" if fused else ")"))
-        roof["launch_us"] = round(kern_us[dom], 2)
+        roof["launch_us"] = round(dom_us, 2)
+        if dom == "gate_up" and fused and not args.gemm_tile:
+            roof["traffic"] = traffic_bytes(w.name)
         roof["algorithmic_bytes"] = int(wk["bytes"])
         roof["algorithmic_flops"] = wk["flops"]
 
@@ -368,6 +415,8 @@ def main():
                    "layers": layers, "weight_copies_rotated": ncopy,
                    "tokens_per_expert": counts.tolist()},
         "ffn_tflops": round(ffn_flops / (ms_per_step * 1e-3) / 1e12, 2),
+        # event pair before each call, from a separate 20-step pass after the
+        # timed region (events between every call add their own gaps)
         "kernels_us": {k: (round(v, 2) if v is not None else None) for k, v in kern_us.items()},
         "host_wall_ms_per_step": round(1e3 * wall / K, 4),
         "roofline": roof,

@@ -118,6 +118,21 @@ __device__ __forceinline__ void static_for(F&& f) {
     }
 }
 
+// Schedule of a register-streamed K-step: like sched_kstep, plus NV global
+// loads (the refill of the registers the fragment's MFMAs just read) after
+// each fragment's MFMAs.
+template <int NM, int NR, int NV, int KK>
+__device__ __forceinline__ void sched_bd_step() {
+    __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);  // fragment 0
+#pragma unroll
+    for (int kk = 0; kk + 1 < KK; ++kk) {
+        sched_spread<NM, NR, 0>();
+        __builtin_amdgcn_sched_group_barrier(0x020, NV, 0);  // VMEM reads
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);  // last fragment
+    __builtin_amdgcn_sched_group_barrier(0x020, NV, 0);
+}
+
 constexpr int GROUP_M = 8;
 constexpr int CPR = 8;  // 16-byte chunks per row per K-step (128 bytes)
 
@@ -375,20 +390,25 @@ struct Epilogue {
     }
 };
 
-template <int BM, int BN, int WGM, int WGN, int NSTAGE, bool F32, int EPI>
+template <int BM, int BN, int WGM, int WGN, int NSTAGE, bool F32, int EPI, int KC = CPR>
 __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     constexpr int NW = WGM * WGN;
     constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int TM = WM / 32, TN = WN / 32;
     constexpr int EPC = F32 ? 4 : 8;       // elements per chunk
-    constexpr int BK = CPR * EPC;          // K elements per step
+    // KC 16-byte chunks of K per row per step: 8 (128 bytes) or 4 (64 bytes,
+    // half-size steps so that twice as many fit in LDS: more bytes in flight
+    // for the same ring).  One DMA instruction moves 1 KB = RPI rows.
+    static_assert(KC == 8 || KC == 4, "chunks per step");
+    constexpr int RPI = 64 / KC;
+    constexpr int BK = KC * EPC;           // K elements per step
     constexpr int ESZ = F32 ? 4 : 2;
-    constexpr int A_INS = BM / 8 / NW;     // DMA instructions per wave per stage
-    constexpr int B_INS = BN / 8 / NW;
+    constexpr int A_INS = BM / RPI / NW;   // DMA instructions per wave per stage
+    constexpr int B_INS = BN / RPI / NW;
     constexpr int LPS = A_INS + B_INS;
-    constexpr int STAGE = (BM + BN) * CPR; // u32x4 slots per stage
+    constexpr int STAGE = (BM + BN) * KC;  // u32x4 slots per stage
     static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile");
-    static_assert(A_INS * 8 * NW == BM && B_INS * 8 * NW == BN, "DMA split");
+    static_assert(A_INS * RPI * NW == BM && B_INS * RPI * NW == BN, "DMA split");
     static_assert(EPI != EPI_GATE_UP_SILU || WN % 64 == 0, "gate/up pairs");
     static_assert(NSTAGE >= 2 && LPS * (NSTAGE - 2) < 64, "stages");
 
@@ -413,50 +433,51 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     const int n_tile = t.n_tile;
     const int64_t n0 = (int64_t)n_tile * BN;
 
-    // A sources.  Instruction i of this wave fills tile rows 8*(wave+NW*i)
-    // .. +7: lane -> row +lane/8, slot lane%8, which holds logical chunk
-    // swz(lane%8, r).  Rows past the expert's block are clamped to its last
+    // A sources.  Instruction i of this wave fills tile rows RPI*(wave+NW*i)
+    // .. +RPI-1: lane -> row +lane/KC, slot lane%KC, which holds logical chunk
+    // swzk(lane%KC, r).  Rows past the expert's block are clamped to its last
     // row (fetched, never stored); with a row map the A row comes from
     // a_rows[row], a valid token row for every row inside the block.
-    const int rsub = lane >> 3;
+    auto swzk = [](int c, int r) { return KC == 8 ? swz(c, r) : c ^ ((r >> 2) & 3); };
+    const int rsub = lane / KC;
     const char* Ab = reinterpret_cast<const char*>(g.A);
     const char* a_src[A_INS];
 #pragma unroll
     for (int i = 0; i < A_INS; ++i) {
-        const int r = 8 * (wave + NW * i) + rsub;
+        const int r = RPI * (wave + NW * i) + rsub;
         int64_t row = m0 + r;
         row = row < m_end ? row : m_end - 1;
         if (g.a_rows) {
             row = g.a_rows[row];
             row = (row >= 0 && row < g.T) ? row : 0;  // a corrupt map stays in bounds
         }
-        a_src[i] = Ab + row * g.lda * ESZ + swz(lane & 7, r) * 16;
+        a_src[i] = Ab + row * g.lda * ESZ + swzk(lane % KC, r) * 16;
     }
-    // B sources: blocked weights, (32-row group, K step) blocks of 4 KB.
-    // Instruction i copies tile rows 8*(wave+NW*i) .. +7 = one contiguous KB
-    // of their group's block; N tiles past the last group reuse it (their
-    // columns are never stored).
-    const int64_t ksteps = g.K / BK;
+    // B sources.  A 32-row group's packed weights form one contiguous stream
+    // along K (4 KB per 128-byte K-step), so a step of the tile copies
+    // KC/2 KB of each group's stream: KB q of the stage's B region is KB
+    // q % (KC/2) of group q / (KC/2).  N tiles past the last group reuse it
+    // (their columns are never stored).
     const char* Bb = reinterpret_cast<const char*>(g.B) + (int64_t)e * g.b_expert_stride * ESZ;
+    const int64_t group_bytes = (g.K / (CPR * EPC)) * 4096;
     const char* b_src[B_INS];
 #pragma unroll
     for (int i = 0; i < B_INS; ++i) {
-        const int r = 8 * (wave + NW * i);
-        int64_t grp = (n0 + r) >> 5;
+        const int q = wave + NW * i;
+        int64_t grp = (n0 >> 5) + q / (KC / 2);
         const int64_t last = (g.N >> 5) - 1;
         grp = grp < last ? grp : last;
-        b_src[i] = Bb + (grp * ksteps * 32 + (r & 31)) * 128 + lane * 16;
+        b_src[i] = Bb + grp * group_bytes + (q % (KC / 2)) * 1024 + lane * 16;
     }
 
     auto issue = [&](int stage, int kt) {
         u32x4* base = lds + stage * STAGE;
-        const int64_t aoff = (int64_t)kt * 128;
-        const int64_t boff = (int64_t)kt * 4096;
+        const int64_t aoff = (int64_t)kt * KC * 16;
+        const int64_t boff = (int64_t)kt * KC * 512;
 #pragma unroll
-        for (int i = 0; i < A_INS; ++i) dma16(a_src[i] + aoff, base + 8 * (wave + NW * i) * CPR);
+        for (int i = 0; i < A_INS; ++i) dma16(a_src[i] + aoff, base + (wave + NW * i) * 64);
 #pragma unroll
-        for (int i = 0; i < B_INS; ++i)
-            dma16(b_src[i] + boff, base + (BM + 8 * (wave + NW * i)) * CPR);
+        for (int i = 0; i < B_INS; ++i) dma16(b_src[i] + boff, base + BM * KC + (wave + NW * i) * 64);
     };
 
     // Output rows of this tile, staged once: the epilogue then needs no
@@ -481,17 +502,17 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     if constexpr (EPI == EPI_RESID_ADD)
         load_residual<TM, TN>(g, acc, wm * WM, n0 + wn * WN, rows, m0, lane);
 
-    const int nk = (int)ksteps;
+    const int nk = (int)(g.K / BK);
 #pragma unroll
     for (int s = 0; s < NSTAGE - 1; ++s)
         if (s < nk) issue(s, s);
 
     const int frow = lane & 31;   // fragment row within a 32-row tile
     const int fhalf = lane >> 5;  // which chunk of the k-pair
-    const int a_row0 = (wm * WM + frow) * CPR;
+    const int a_row0 = (wm * WM + frow) * KC;
     // B fragments sit in LDS as packed: 32-row group G of the tile at slot
-    // BM*CPR + 256*G, fragment kk at +64*kk, one slot per lane.
-    const int b_frag0 = BM * CPR + wn * TN * 256 + lane;
+    // BM*KC + 32*KC*G, fragment kk of the step at +64*kk, one slot per lane.
+    const int b_frag0 = BM * KC + wn * TN * 32 * KC + lane;
 
     for (int kt = 0; kt < nk; ++kt) {
         if (kt + NSTAGE - 2 < nk)
@@ -504,16 +525,16 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
         const u32x4* S = lds + (kt % NSTAGE) * STAGE;
         u32x4 af[2][TM], bfr[2][TN];
         auto frag = [&](int buf, int kk) {
-            const int ch = swz(2 * kk + fhalf, frow);
+            const int ch = swzk(2 * kk + fhalf, frow);
 #pragma unroll
-            for (int i = 0; i < TM; ++i) af[buf][i] = S[a_row0 + i * 32 * CPR + ch];
+            for (int i = 0; i < TM; ++i) af[buf][i] = S[a_row0 + i * 32 * KC + ch];
 #pragma unroll
-            for (int j = 0; j < TN; ++j) bfr[buf][j] = S[b_frag0 + j * 256 + kk * 64];
+            for (int j = 0; j < TN; ++j) bfr[buf][j] = S[b_frag0 + j * 32 * KC + kk * 64];
         };
         frag(0, 0);
 #pragma unroll
-        for (int kk = 0; kk < CPR / 2; ++kk) {
-            if (kk + 1 < CPR / 2) frag((kk + 1) & 1, kk + 1);
+        for (int kk = 0; kk < KC / 2; ++kk) {
+            if (kk + 1 < KC / 2) frag((kk + 1) & 1, kk + 1);
             const int cb = kk & 1;
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
@@ -533,7 +554,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
                 }
             }
         }
-        sched_kstep<TM * TN * (F32 ? 4 : 1), TM + TN, CPR / 2>();
+        sched_kstep<TM * TN * (F32 ? 4 : 1), TM + TN, KC / 2>();
     }
 
     Epi::run(g, acc, wm, wn, n0, rows, m0, crow, lds, tid, NW * 64);
@@ -687,6 +708,20 @@ struct BdTile {
 
     const int frow = lane & 31;
     const int fhalf = lane >> 5;
+    // Loads of K-step kt+S issued right after the MFMAs that free their
+    // registers, spread over the step, so the address unit streams while the
+    // matrix cores work instead of taking every load at the end of the step.
+    constexpr int KK = CPR / 2;
+    auto refill = [&](auto sc, int kt, int kk) {
+        constexpr int sl = decltype(sc)::value;
+        kt = kt < nk ? kt : nk - 1;
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+            bq[sl][j][kk] = *reinterpret_cast<const u32x4*>(b_src[j] + (int64_t)kt * 4096 + kk * 1024);
+#pragma unroll
+        for (int i = kk * A_INS / KK; i < (kk + 1) * A_INS / KK; ++i)
+            aq[sl][i] = *reinterpret_cast<const u32x4*>(a_src[i] + (int64_t)kt * 128);
+    };
     auto step = [&](auto sc, int kt) {
         constexpr int s = decltype(sc)::value;
         const u32x4* L = lds + (kt & 1) * STAGE;
@@ -698,8 +733,8 @@ struct BdTile {
         };
         frag(0, 0);
 #pragma unroll
-        for (int kk = 0; kk < CPR / 2; ++kk) {
-            if (kk + 1 < CPR / 2) frag((kk + 1) & 1, kk + 1);
+        for (int kk = 0; kk < KK; ++kk) {
+            if (kk + 1 < KK) frag((kk + 1) & 1, kk + 1);
             const int cb = kk & 1;
 #pragma unroll
             for (int i = 0; i < TM; ++i)
@@ -717,11 +752,9 @@ struct BdTile {
                             __builtin_bit_cast(bf16x8, bq[s][j][kk]), acc[i][j], 0, 0, 0);
                     }
                 }
+            refill(sc, kt + S, kk);
         }
-        sched_kstep<TM * TN * (F32 ? 4 : 1), TM, CPR / 2>();
-        // Weights of K-step kt+S into the slot just consumed (activations of
-        // that slot already went to LDS one step earlier).
-        load(sc, kt + S);
+        sched_bd_step<TM * TN * (F32 ? 4 : 1), TM, TN + A_INS / KK, KK>();
         store_a(std::integral_constant<int, (s + 1) % S>{}, (kt + 1) & 1);
         __syncthreads();
     };
@@ -761,7 +794,7 @@ inline hipError_t launch_bd(GemmArgs g, hipStream_t s) {
     return hipGetLastError();
 }
 
-template <int BM, int BN, int WGM, int WGN, int NSTAGE, bool F32, int EPI>
+template <int BM, int BN, int WGM, int WGN, int NSTAGE, bool F32, int EPI, int KC = CPR>
 inline hipError_t launch_cfg(GemmArgs g, hipStream_t s) {
     g.n_tiles = (int)ceil_div(g.N, BN);
     int64_t mt = (g.T + (int64_t)g.E * (BM - 1)) / BM;
@@ -770,7 +803,7 @@ inline hipError_t launch_cfg(GemmArgs g, hipStream_t s) {
     const int64_t blocks = round_up((int64_t)g.n_tiles * g.m_tiles_max, 8);
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    k_grouped_gemm<BM, BN, WGM, WGN, NSTAGE, F32, EPI>
+    k_grouped_gemm<BM, BN, WGM, WGN, NSTAGE, F32, EPI, KC>
         <<<dim3((unsigned)blocks), dim3(WGM * WGN * 64), 0, s>>>(g);
     return hipGetLastError();
 }
@@ -797,7 +830,12 @@ enum TileCfg {
     TILE_BD_32x256 = 14,   // 4 waves of 32x64, 4 K-steps
     TILE_BD_32x128 = 15,   // 2 waves of 32x64, 6 K-steps
     TILE_BD_256x256 = 16,  // 4 waves of 256x64, 2 K-steps
-    TILE_LAST = TILE_BD_256x256,
+    // Both operands in LDS, 64-byte K steps (twice as many steps in flight):
+    TILE_256x256_K32 = 17,  // 2x4 waves of 128x64, 4 half steps, 128 KB
+    TILE_128x256_K32 = 18,  // 2x4 waves of 64x64, 6 half steps, 144 KB
+    TILE_BD_128x256_S5 = 19,  // as 12, 5 K-steps in flight
+    TILE_BD_128x256_S6 = 20,  // as 12, 6 K-steps in flight
+    TILE_LAST = TILE_BD_128x256_S6,
 };
 
 // Launches one tile configuration (instantiated per element type and
@@ -815,6 +853,8 @@ hipError_t launch_tile(int tile, GemmArgs g, hipStream_t s) {
         case TILE_256x256_W4: return launch_cfg<256, 256, 2, 2, 2, F32, EPI>(g, s);
         case TILE_256x128_W4: return launch_cfg<256, 128, 2, 2, 3, F32, EPI>(g, s);
         case TILE_128x256_W4: return launch_cfg<128, 256, 1, 4, 3, F32, EPI>(g, s);
+        case TILE_256x256_K32: return launch_cfg<256, 256, 2, 4, 4, F32, EPI, 4>(g, s);
+        case TILE_128x256_K32: return launch_cfg<128, 256, 2, 4, 6, F32, EPI, 4>(g, s);
         default: break;
     }
     if constexpr (!F32) {
@@ -824,6 +864,8 @@ hipError_t launch_tile(int tile, GemmArgs g, hipStream_t s) {
             case TILE_BD_32x256: return launch_bd<32, 4, 2, 4, F32, EPI>(g, s);
             case TILE_BD_32x128: return launch_bd<32, 2, 2, 6, F32, EPI>(g, s);
             case TILE_BD_256x256: return launch_bd<256, 4, 2, 2, F32, EPI>(g, s);
+            case TILE_BD_128x256_S5: return launch_bd<128, 4, 2, 5, F32, EPI>(g, s);
+            case TILE_BD_128x256_S6: return launch_bd<128, 4, 2, 6, F32, EPI>(g, s);
             default: break;
         }
     }
