@@ -1,25 +1,18 @@
 // Grouping tokens by expert (the per-expert queues of the expert-aware
 // batching, Sec. 4.2 Alg. 1) and the row moves around the expert FFN.
 //
-// k_group: one 1024-thread workgroup.
-//   1. histogram of ids in LDS (order-free, so LDS atomics are exact);
-//   2. exclusive scan -> counts, offsets;
-//   3. stable ranks, 1024 tokens per round: each wave finds, by eight
-//      ballots over the id bits, the lanes that share its id (a match mask);
-//      rank within the wave = popcount of the lower matching lanes; per-wave
-//      per-expert counts are scanned across the 16 waves in wave order, so
-//      the rank of token t is #{t' < t with the same id}, i.e. a stable
-//      counting sort, with no atomics in the ordering.
+// k_group: one 1024-thread workgroup running GroupBlock (group_block.hpp):
+//   histogram, exclusive scan, stable counting-sort ranks.
 // k_move_rows: dst[r] = src[idx[r]] (zero row if idx[r] < 0), 16-byte
 //   vector copies, one row per 64-lane wave slice; serves both the gather
 //   into grouped order (idx = perm) and the ungroup (idx = inv_perm).
 #include "common.hpp"
+#include "group_block.hpp"
 #include "internal.hpp"
 
 namespace readme {
 
 constexpr int kGroupThreads = 1024;
-constexpr int kGroupWaves = kGroupThreads / 64;
 
 __global__ __launch_bounds__(kGroupThreads) void k_group(int T, int E, int nbits,
                                                          const int32_t* __restrict__ ids,
@@ -27,71 +20,8 @@ __global__ __launch_bounds__(kGroupThreads) void k_group(int T, int E, int nbits
                                                          int32_t* __restrict__ offsets,
                                                          int32_t* __restrict__ perm,
                                                          int32_t* __restrict__ inv_perm) {
-    __shared__ int hist[README_MAX_EXPERTS];
-    __shared__ int cursor[README_MAX_EXPERTS];
-    __shared__ int wcnt[kGroupWaves][README_MAX_EXPERTS];
-    __shared__ int wbase[kGroupWaves][README_MAX_EXPERTS];
-    const int tid = threadIdx.x;
-    const int wave = tid >> 6;
-
-    for (int i = tid; i < README_MAX_EXPERTS; i += kGroupThreads) hist[i] = 0;
-    for (int i = tid; i < kGroupWaves * README_MAX_EXPERTS; i += kGroupThreads)
-        (&wcnt[0][0])[i] = 0;
-    __syncthreads();
-    for (int t = tid; t < T; t += kGroupThreads) {
-        const int e = ids[t];
-        if (e >= 0 && e < E) atomicAdd(&hist[e], 1);
-    }
-    __syncthreads();
-    if (tid == 0) {
-        int s = 0;
-        offsets[0] = 0;
-        for (int e = 0; e < E; ++e) {
-            cursor[e] = s;
-            counts[e] = hist[e];
-            s += hist[e];
-            offsets[e + 1] = s;
-        }
-        hist[0] = s;  // routed tokens
-    }
-    __syncthreads();
-    const int routed = hist[0];
-
-    for (int base = 0; base < T; base += kGroupThreads) {
-        const int t = base + tid;
-        const int e = t < T ? ids[t] : -1;
-        const bool valid = e >= 0 && e < E;
-        uint64_t match = __ballot(valid);
-        for (int b = 0; b < nbits; ++b) {
-            const bool bit = valid && ((e >> b) & 1);
-            const uint64_t ones = __ballot(bit);
-            match &= bit ? ones : ~ones;
-        }
-        const int rank = __popcll(match & lanemask_lt());
-        if (valid && rank == 0) wcnt[wave][e] = __popcll(match);
-        __syncthreads();
-        for (int x = tid; x < E; x += kGroupThreads) {
-            int s = cursor[x];
-            for (int w = 0; w < kGroupWaves; ++w) {
-                wbase[w][x] = s;
-                s += wcnt[w][x];
-                wcnt[w][x] = 0;
-            }
-            cursor[x] = s;
-        }
-        __syncthreads();
-        if (t < T) {
-            if (valid) {
-                const int j = wbase[wave][e] + rank;
-                perm[j] = t;
-                inv_perm[t] = j;
-            } else {
-                inv_perm[t] = -1;
-            }
-        }
-        __syncthreads();
-    }
-    for (int j = routed + tid; j < T; j += kGroupThreads) perm[j] = -1;
+    __shared__ int smem[GroupBlock<kGroupThreads>::SMEM_INTS];
+    GroupBlock<kGroupThreads>::run(T, E, nbits, ids, counts, offsets, perm, inv_perm, smem);
 }
 
 hipError_t launch_group(int64_t T, int E, const int32_t* ids, int32_t* counts, int32_t* offsets,

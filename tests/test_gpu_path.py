@@ -331,3 +331,4 @@ def test_fused_leaves_unrouted_rows_untouched(L):
     assert (yh[routed] == rh[routed]).all()
     assert (wl.bf16_bits_to_f32(yh[~routed]) == 7.0).all()
 
+
