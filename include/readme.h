@@ -161,8 +161,10 @@ int64_t readme_padded_intermediate(int64_t I);
  *     1 = 256x256, 2 = 256x128, 3 = 128x128, 4 = 128x256, 5 = 64x128,
  *     6 = 32x128, 7 = 32x64 (deep pipeline), 8 = 32x128 (deep pipeline),
  *     9 = 256x256, 10 = 256x128, 11 = 128x256 (four waves, larger wave tiles)
+ *     17 = 256x256, 18 = 128x256 (half-size K steps, deeper pipeline)
  *   weights streamed straight into registers (bf16; fp32 runs tile 6):
- *     12 = 128x256, 13 = 64x256, 14 = 32x256, 15 = 32x128 (deep pipeline)
+ *     12 = 128x256, 13 = 64x256, 14 = 32x256, 15 = 32x128 (deep pipeline),
+ *     16 = 256x256, 19 = 128x256 (5 stages), 20 = 128x256 (6 stages)
  *   (rows of tokens x columns of outputs)
  * Results do not depend on the tile beyond fp32 summation order.  Returns
  * README_ERR_ARG for any other value.  Not synchronised with calls in

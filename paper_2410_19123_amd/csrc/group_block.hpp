@@ -1,6 +1,6 @@
 // The grouping step (histogram, exclusive scan, stable counting-sort ranks)
-// as one workgroup's routine, shared by k_group and the router's fused
-// grouping (route.hip).  NT threads; smem: SMEM_INTS ints of LDS.
+// as one workgroup's routine (k_group runs it; any kernel that ends with the
+// grouping of its ids can too).  NT threads; smem: SMEM_INTS ints of LDS.
 //   1. histogram of ids in LDS (order-free, so LDS atomics are exact);
 //   2. exclusive scan -> counts, offsets;
 //   3. stable ranks, NT tokens per round: each wave finds, by ballots over
