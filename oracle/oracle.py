@@ -146,6 +146,26 @@ def moe_ffn(x_g, offsets, w_gate, w_up, w_down, rows=None) -> np.ndarray:
     return y
 
 
+def moe_ffn_permanent(x_g, offsets, w_gate, w_up, w_down, p_gate, p_up, p_down,
+                      rows=None) -> np.ndarray:
+    """fp64 FFN of a layer with a permanent expert (Sec. 3: a set of neurons
+    that every token activates, beside the routed expert of Eq. 2):
+    y[j] = F_{e_j}(x_g[j]) + F_perm(x_g[j]), F_perm the SwiGLU FFN with
+    p_gate[P][d], p_up[P][d], p_down[d][P].  Both terms are moe_ffn's fp64
+    evaluation; the permanent one as a single expert whose block is every
+    routed row."""
+    x_g = np.ascontiguousarray(x_g)
+    E = w_gate.shape[0]
+    routed = moe_ffn(x_g, offsets, w_gate, w_up, w_down, rows=rows)
+    n = int(offsets[E])
+    if rows is None:
+        rows = np.arange(n)
+    everyone = np.array([0, n], np.int32)
+    perm_part = moe_ffn(x_g, everyone, p_gate[None], p_up[None],
+                        np.ascontiguousarray(p_down)[None], rows=rows)
+    return routed + perm_part
+
+
 def layer(x_res, offsets, w_gate, w_up, w_down, eps=1e-5, rows=None,
           want_xn=False):
     """One decode-stack layer's FFN output (the residual increment), fp64."""
@@ -182,11 +202,12 @@ def f32_to_bf16(a: np.ndarray) -> np.ndarray:
     return out
 
 
-def full_path(x, w_router, bias, w_gate, w_up, w_down, ids=None):
+def full_path(x, w_router, bias, w_gate, w_up, w_down, ids=None, permanent=None):
     """route -> group -> gather -> expert FFN -> ungroup, one layer.
 
     Returns a dict with ids, logits, counts, offsets, perm, inv_perm, x_g,
-    y_g (fp64) and y (fp64, token order).  ``ids`` given skips the router.
+    y_g (fp64) and y (fp64, token order).  ``ids`` given skips the router;
+    ``permanent`` = (p_gate, p_up, p_down) adds the permanent expert.
     """
     E = w_gate.shape[0]
     logits = None
@@ -196,7 +217,11 @@ def full_path(x, w_router, bias, w_gate, w_up, w_down, ids=None):
     x_g = gather(x, perm)
     n = int(offsets[E])
     y_g = np.zeros(x.shape, np.float64)
-    y_g[:n] = moe_ffn(x_g, offsets, w_gate, w_up, w_down, rows=np.arange(n))
+    if permanent is None:
+        y_g[:n] = moe_ffn(x_g, offsets, w_gate, w_up, w_down, rows=np.arange(n))
+    else:
+        y_g[:n] = moe_ffn_permanent(x_g, offsets, w_gate, w_up, w_down, *permanent,
+                                    rows=np.arange(n))
     y = ungroup(y_g, inv)
     return dict(ids=ids, logits=logits, counts=counts, offsets=offsets,
                 perm=perm, inv_perm=inv, x_g=x_g, y_g=y_g, y=y)

@@ -47,7 +47,8 @@ class Workload:
     T tokens of width d, E experts each a SwiGLU FFN of intermediate width I,
     ``layers`` stacked layers sharing one routing (the pre-gating router runs
     once per step).  ``router`` is False when expert ids are given per request
-    instead of computed.
+    instead of computed.  ``P`` > 0 adds a permanent expert of P intermediate
+    neurons that every token passes through.
     """
     name: str
     T: int
@@ -55,6 +56,7 @@ class Workload:
     E: int
     I: int
     dtype: str            # "f32" or "bf16"
+    P: int = 0
     layers: int = 1
     router: bool = True
     bias: str = "none"    # "none" | "zipf1" | "skew40_zipf1.2"
@@ -89,6 +91,12 @@ WORKLOADS = {
         bias="skew40_zipf1.2",
         description="prefill-scale skewed layer: T=16384, d=4096, E=16, "
                     "I=688, expert 0 ~40%, rest Zipf(1.2)"),
+    "llama7b_layer_perm": Workload(
+        "llama7b_layer_perm", T=2048, d=4096, E=8, I=1376, P=1376, dtype="bf16",
+        bias="zipf1",
+        description="Llama-7B-shaped MoE layer with a permanent expert: T=2048, "
+                    "d=4096, E=8 routed experts of I=1376 plus P=1376 neurons "
+                    "every token passes through, Zipf(1.0) router bias"),
     "wide_requests": Workload(
         "wide_requests", T=8192, d=8192, E=8, I=3584, dtype="bf16",
         router=False, requests=256,
@@ -185,34 +193,45 @@ def make_request_ids(w: Workload, seed: int = 0) -> np.ndarray:
     return np.repeat(req, per).astype(np.int32)
 
 
-def make_experts(w: Workload, seed: int = 0, layer: int = 0):
-    """Expert weights of one layer, sliced from one dense SwiGLU FFN.
-
-    The dense FFN has intermediate width D = E*I; expert e owns intermediate
-    columns [e*I, (e+1)*I).  Returns (w_gate[E][I][d], w_up[E][I][d],
-    w_down[E][d][I]).
-    """
-    D = w.E * w.I
-    wg = normal((D, w.d), 0.02, [seed, TAG_GATE, layer]).reshape(w.E, w.I, w.d)
-    wu = normal((D, w.d), 0.02, [seed, TAG_UP, layer]).reshape(w.E, w.I, w.d)
-    wd_dense = normal((w.d, D), 0.02, [seed, TAG_DOWN, layer])
-    wd = np.ascontiguousarray(wd_dense.reshape(w.d, w.E, w.I).transpose(1, 0, 2))
-    return _cast(w, wg), _cast(w, wu), _cast(w, wd)
-
-
 def make_dense(w: Workload, seed: int = 0, layer: int = 0):
-    """The dense FFN the experts were sliced from: (W_gate[D][d], W_up[D][d],
-    W_down[d][D]) with D = E*I, in the workload's dtype."""
-    D = w.E * w.I
+    """The dense FFN the experts are sliced from: (W_gate[D][d], W_up[D][d],
+    W_down[d][D]) with D = E*I + P, in the workload's dtype."""
+    D = w.E * w.I + w.P
     wg = normal((D, w.d), 0.02, [seed, TAG_GATE, layer])
     wu = normal((D, w.d), 0.02, [seed, TAG_UP, layer])
     wd = normal((w.d, D), 0.02, [seed, TAG_DOWN, layer])
     return _cast(w, wg), _cast(w, wu), _cast(w, wd)
 
 
+def make_experts(w: Workload, seed: int = 0, layer: int = 0):
+    """Routed expert weights of one layer, sliced from one dense SwiGLU FFN.
+
+    The dense FFN has intermediate width D = E*I + P; expert e owns
+    intermediate columns [e*I, (e+1)*I) (the permanent expert, if any, the
+    last P).  Returns (w_gate[E][I][d], w_up[E][I][d], w_down[E][d][I]).
+    """
+    dg, du, dd = make_dense(w, seed, layer)
+    n = w.E * w.I
+    wg = dg[:n].reshape(w.E, w.I, w.d)
+    wu = du[:n].reshape(w.E, w.I, w.d)
+    wd = np.ascontiguousarray(dd[:, :n].reshape(w.d, w.E, w.I).transpose(1, 0, 2))
+    return np.ascontiguousarray(wg), np.ascontiguousarray(wu), wd
+
+
+def make_permanent(w: Workload, seed: int = 0, layer: int = 0):
+    """The permanent expert of one layer: intermediate columns [E*I, E*I + P)
+    of the same dense FFN.  Returns (p_gate[P][d], p_up[P][d], p_down[d][P])."""
+    if w.P <= 0:
+        raise ValueError(f"workload {w.name} has no permanent expert")
+    dg, du, dd = make_dense(w, seed, layer)
+    n = w.E * w.I
+    return (np.ascontiguousarray(dg[n:]), np.ascontiguousarray(du[n:]),
+            np.ascontiguousarray(dd[:, n:]))
+
+
 def flops_per_layer(w: Workload) -> float:
-    """Algorithmic FLOP of the expert FFN of one layer: 6*T*d*I."""
-    return 6.0 * w.T * w.d * w.I
+    """Algorithmic FLOP of the expert FFN of one layer: 6*T*d*(I + P)."""
+    return 6.0 * w.T * w.d * (w.I + w.P)
 
 
 def describe(w: Workload) -> str:
@@ -222,5 +241,5 @@ def describe(w: Workload) -> str:
 __all__ = [
     "Workload", "WORKLOADS", "normal", "to_bf16_bits", "bf16_bits_to_f32",
     "router_bias", "make_x", "make_router", "make_request_ids",
-    "make_experts", "make_dense", "flops_per_layer", "describe", "SKEW_BIAS0",
+    "make_experts", "make_permanent", "make_dense", "flops_per_layer", "describe", "SKEW_BIAS0",
 ]
