@@ -91,13 +91,19 @@ class Path:
         self.yg = torch.empty_like(self.x)
         self.y = torch.empty_like(self.x)
         self.Ip = _lib.readme_padded_intermediate(w.I)
-        self.h = torch.empty(w.T, self.Ip, dtype=self.x.dtype, device=dev)
+        # h holds the routed expert's neurons, then the permanent expert's
+        # (P / I slices of one expert's width).
+        self.h = torch.empty(w.T, (1 + w.P // w.I) * self.Ip, dtype=self.x.dtype, device=dev)
         self.packed = []
         for layer in range(w.layers):
-            wg, wu, wd = wl.make_experts(w, seed, layer=layer)
-            p = _lib.readme_pack_experts(*U.weights_to_dev(wg, wu, wd))
+            wts = U.weights_to_dev(*wl.make_experts(w, seed, layer=layer))
+            if w.P:
+                p = _lib.readme_pack_experts_permanent(
+                    *wts, *U.weights_to_dev(*wl.make_permanent(w, seed, layer=layer)))
+            else:
+                p = _lib.readme_pack_experts(*wts)
             self.packed.append(p)
-            del wg, wu, wd
+            del wts
         if w.layers == 1:
             for _ in range(copies - 1):
                 self.packed.append(self.packed[0].clone())
@@ -175,12 +181,22 @@ class Path:
 
     def gate_up_gather(self, k):
         P, w = self.P, self.w
+        if w.P:
+            self._ok(self.lib.readme_moe_gate_up_permanent_gather(
+                self.dt, w.T, w.d, w.E, w.I, w.P, P(self.x), P(self.perm), P(self.offsets),
+                P(self.packed[k]), P(self.h), self.stream), "gate_up_permanent_gather")
+            return
         self._ok(self.lib.readme_moe_gate_up_gather(
             self.dt, w.T, w.d, w.E, w.I, P(self.x), P(self.perm), P(self.offsets),
             P(self.packed[k]), P(self.h), self.stream), "gate_up_gather")
 
     def down_scatter(self, k):
         P, w = self.P, self.w
+        if w.P:
+            self._ok(self.lib.readme_moe_down_permanent_scatter(
+                self.dt, w.T, w.d, w.E, w.I, w.P, P(self.h), P(self.perm), P(self.offsets),
+                P(self.packed[k]), P(self.y), self.stream), "down_permanent_scatter")
+            return
         self._ok(self.lib.readme_moe_down_scatter(
             self.dt, w.T, w.d, w.E, w.I, P(self.h), P(self.perm), P(self.offsets),
             P(self.packed[k]), P(self.y), self.stream), "down_scatter")
@@ -203,7 +219,7 @@ class Path:
 # HBM traffic of the dominant kernel, per launch, from two rocprofv3 --pmc runs of
 # this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each scaled by what
 # the same counter reads for a plain 1 GiB device copy in the same run (--copy-probe:
-# FETCH_SIZE reads 524313 KiB for it, so reads scale by 1.99991; WRITE_SIZE reads
+# FETCH_SIZE reads 524307 KiB for it, so reads scale by 1.99993; WRITE_SIZE reads
 # exactly 1 GiB, factor 1).  Valid only for the sources the counters were taken
 # with: the entry carries their sha256 and is dropped (traffic null) once any of
 # them changes.
@@ -211,8 +227,8 @@ TRAFFIC_SOURCES = ["csrc/gemm_kernels.hpp", "csrc/gemm.hip", "csrc/gemm_bf16_gat
                    "csrc/common.hpp", "csrc/internal.hpp", "csrc/pack.hip", "workloads.py"]
 TRAFFIC = {
     # workload: (sources sha256, read bytes, written bytes) per gate/up launch
-    "llama7b_layer": ("d66f8f29d7c28f79e99540d1100566760b955655e1baa95fc40744ef998be655",
-                      234296042, 5767168),
+    "llama7b_layer": ("be3bacaaaf972b4b8acad7bbc857544e4cd0c9658a2412ecea24a012d65054c5",
+                      234297971, 5767168),
 }
 
 
@@ -250,12 +266,14 @@ def algorithmic(w: wl.Workload, counts: np.ndarray, fused: bool = False) -> dict
                           flops=6.0 * n * d * I * L),
             "ungroup": dict(bytes=2 * T * d * 4 + 4 * T, flops=0.0),
         }
+    P = w.P  # permanent expert: P more neurons for every routed token
     return {
         "route": dict(bytes=T * d * s + E * d * s + 4 * T, flops=2.0 * T * d * E),
         "group": dict(bytes=4 * T + 8 * T + 8 * E + (0 if fused else 2 * n * d * s), flops=0.0),
-        "gate_up": dict(bytes=active * 2 * I * d * s + n * d * s + n * I * s,
-                        flops=4.0 * n * d * I),
-        "down": dict(bytes=active * I * d * s + n * I * s + n * d * s, flops=2.0 * n * d * I),
+        "gate_up": dict(bytes=(active * I + P) * 2 * d * s + n * d * s + n * (I + P) * s,
+                        flops=4.0 * n * d * (I + P)),
+        "down": dict(bytes=(active * I + P) * d * s + n * (I + P) * s + n * d * s,
+                     flops=2.0 * n * d * (I + P)),
         "ungroup": dict(bytes=2 * T * d * s + 4 * T, flops=0.0),
     }
 
@@ -269,12 +287,13 @@ def cpu_baseline(w: wl.Workload, target_s: float) -> dict:
     x_all = wl.make_x(w)
     wr, b = wl.make_router(w)
     wg, wu, wd = wl.make_experts(w)
+    perm_expert = wl.make_permanent(w) if w.P else None
     ids_all = None if w.router else wl.make_request_ids(w)
 
     def run(S):
         ids = None if ids_all is None else ids_all[:S]
         t0 = time.perf_counter()
-        oracle.full_path(x_all[:S], wr, b, wg, wu, wd, ids=ids)
+        oracle.full_path(x_all[:S], wr, b, wg, wu, wd, ids=ids, permanent=perm_expert)
         return time.perf_counter() - t0
 
     S = min(w.T, 16)
@@ -287,7 +306,8 @@ def cpu_baseline(w: wl.Workload, target_s: float) -> dict:
     return {"value": reps * S / total, "unit": "tokens/s", "cores": oracle.threads(),
             "kind": "oracle",
             "sample": f"first {S} of {w.T} tokens of the {w.name} workload, full path "
-                      f"(route, group, gather, fp64 expert FFN, ungroup), {reps} pass(es), "
+                      f"(route, group, gather, fp64 expert FFN"
+                      f"{' + permanent expert' if w.P else ''}, ungroup), {reps} pass(es), "
                       f"{total:.1f} s"}
 
 
@@ -303,7 +323,10 @@ def main():
         sys.exit(1)
 
     w = wl.WORKLOADS[args.workload]
-    packed_bytes = 3 * w.E * (-(-w.I // 64) * 64) * w.d * w.elem_bytes
+    if w.P and args.unfused:
+        print("bench.py: the permanent-expert workload runs the fused path only", file=sys.stderr)
+        sys.exit(2)
+    packed_bytes = 3 * (w.E + w.P // w.I) * (-(-w.I // 64) * 64) * w.d * w.elem_bytes
     copies = args.weight_copies or max(4, -(-(1 << 30) // packed_bytes))
     path = Path(w, copies)
     if args.gemm_tile:
@@ -370,7 +393,7 @@ def main():
     value = w.T * K / (gpu_ms / 1e3)  # tokens/s through one step
     if layers > 1:
         value = value * layers       # per MoE layer
-    ffn_flops = 6.0 * int(counts.sum()) * w.d * w.I * layers
+    ffn_flops = 6.0 * int(counts.sum()) * w.d * (w.I + w.P) * layers
 
     roof = None
     if dom_us:
@@ -389,6 +412,7 @@ def main():
                     "frac": round(ach / pk, 4), "traffic": None}
         roof["kernel"] = ("readme_moe_ffn_stack (all layers)" if layers > 1
                           else "k_grouped_gemm (gate/up + SiLU*mul"
+                          + (", permanent expert as extra row groups" if w.P else "")
                           + (", rows gathered through perm)" if fused else ")"))
         roof["launch_us"] = round(dom_us, 2)
         if dom == "gate_up" and fused and not args.gemm_tile:
@@ -409,7 +433,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32" if w.dtype == "f32" else "bf16",
         "data": "synthetic (seeded N(0,1) tokens, N(0,0.02) weights)",
-        "config": {"workload": w.name, "T": w.T, "d": w.d, "E": w.E, "I": w.I,
+        "config": {"workload": w.name, "T": w.T, "d": w.d, "E": w.E, "I": w.I, "P": w.P,
                    "gemm_tile": args.gemm_tile,
                    "row_moves": "separate" if args.unfused or layers > 1 else "fused into GEMMs",
                    "layers": layers, "weight_copies_rotated": ncopy,

@@ -65,6 +65,7 @@ typedef int32_t readme_dtype;
 #define README_BF16 1
 
 #define README_MAX_EXPERTS 256
+#define README_MAX_PERMANENT_SLICES 16
 
 /* Human-readable name of a status code (static storage). */
 const char *readme_status_string(readme_status s);
@@ -251,6 +252,86 @@ readme_status readme_moe_down_scatter(readme_dtype dt, int64_t T, int64_t d,
                                       const int32_t *offsets,
                                       const void *packed, void *y,
                                       void *stream);
+
+/*
+ * Permanent expert (Sec. 3): neurons that every token activates, beside its
+ * routed expert.  A layer then computes, for every routed token,
+ *   y = F_{e_t}(x) + F_perm(x),
+ * F_perm the SwiGLU FFN of the permanent neurons, unweighted like the routed
+ * term (Eq. 2 with K = 1).  The permanent width P is a whole number of expert
+ * widths, P = S * I with 0 <= S <= README_MAX_PERMANENT_SLICES (S = 0 is the
+ * plain layer), and is held as S slices of one expert's shape.
+ *
+ * readme_pack_experts_permanent -- one-time repack as readme_pack_experts,
+ *   plus the permanent expert: p_gate [P][d], p_up [P][d], p_down [d][P]
+ *   (dtype dt, device), slice j = neurons j*I .. j*I+I-1.  packed must hold
+ *   readme_packed_experts_permanent_bytes(dt, E, d, I, P) bytes (0 for
+ *   invalid arguments).  Not timed on the hot path.
+ * readme_moe_ffn_permanent -- readme_moe_ffn with the permanent expert:
+ *   y_grouped[j] = F_e(x_grouped[j]) + F_perm(x_grouped[j]) for
+ *   j < offsets[E]; rows past offsets[E] are not written.
+ * readme_moe_ffn_permanent_fused -- the same with the row moves folded in,
+ *   as readme_moe_ffn_fused: activations read from x[perm[j]] (token order),
+ *   output row j written to y[perm[j]]; rows of unrouted tokens are not
+ *   written.
+ *   workspace >= readme_moe_ffn_permanent_workspace_bytes(dt, T, I, P)
+ *   bytes: h [T][(1+S)*Ip], the routed expert's neurons then each slice's.
+ * Two launches: the gate/up GEMM treats the slices as S more row groups
+ * over all routed rows; the down GEMM runs one K loop over the routed and
+ * the permanent neurons of each row, so the sum is formed in fp32 and
+ * rounded once.  Requirements and errors as readme_moe_ffn; P not a multiple
+ * of I, or more than README_MAX_PERMANENT_SLICES slices, is
+ * README_ERR_UNSUPPORTED, P < 0 README_ERR_ARG.
+ */
+/*
+ * The two halves of readme_moe_ffn_permanent_fused, for callers that time or
+ * overlap them (h [T][(1+S)*Ip] dt, S = P / I, as in the workspace above):
+ *   readme_moe_gate_up_permanent_gather: h[j] = the routed expert's and each
+ *     permanent slice's silu(g) * u of x[perm[j]] (pad columns 0);
+ *   readme_moe_down_permanent_scatter: y[perm[j]] = W_down^e h[j][routed] +
+ *     W_down^perm h[j][permanent], one fp32 sum rounded once.
+ */
+readme_status readme_moe_gate_up_permanent_gather(readme_dtype dt, int64_t T,
+                                                  int64_t d, int32_t E, int64_t I,
+                                                  int64_t P, const void *x,
+                                                  const int32_t *perm,
+                                                  const int32_t *offsets,
+                                                  const void *packed, void *h,
+                                                  void *stream);
+readme_status readme_moe_down_permanent_scatter(readme_dtype dt, int64_t T,
+                                                int64_t d, int32_t E, int64_t I,
+                                                int64_t P, const void *h,
+                                                const int32_t *perm,
+                                                const int32_t *offsets,
+                                                const void *packed, void *y,
+                                                void *stream);
+size_t readme_packed_experts_permanent_bytes(readme_dtype dt, int32_t E, int64_t d,
+                                             int64_t I, int64_t P);
+readme_status readme_pack_experts_permanent(readme_dtype dt, int32_t E, int64_t d,
+                                            int64_t I, int64_t P,
+                                            const void *w_gate, const void *w_up,
+                                            const void *w_down, const void *p_gate,
+                                            const void *p_up, const void *p_down,
+                                            void *packed, size_t packed_bytes,
+                                            void *stream);
+size_t readme_moe_ffn_permanent_workspace_bytes(readme_dtype dt, int64_t T,
+                                                int64_t I, int64_t P);
+readme_status readme_moe_ffn_permanent(readme_dtype dt, int64_t T, int64_t d,
+                                       int32_t E, int64_t I, int64_t P,
+                                       const void *x_grouped,
+                                       const int32_t *offsets,
+                                       const void *packed, void *y_grouped,
+                                       void *workspace, size_t workspace_bytes,
+                                       void *stream);
+readme_status readme_moe_ffn_permanent_fused(readme_dtype dt, int64_t T,
+                                             int64_t d, int32_t E, int64_t I,
+                                             int64_t P, const void *x,
+                                             const int32_t *perm,
+                                             const int32_t *offsets,
+                                             const void *packed, void *y,
+                                             void *workspace,
+                                             size_t workspace_bytes,
+                                             void *stream);
 
 /*
  * readme_ungroup -- rows back to token order: y[t] = y_grouped[inv_perm[t]],

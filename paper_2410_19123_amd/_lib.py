@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libreadme.so")
 
 README_F32, README_BF16 = 0, 1
 README_MAX_EXPERTS = 256
+README_MAX_PERMANENT_SLICES = 16
 
 _STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported size or type",
            3: "buffer smaller than required", 4: "HIP launch failed"}
@@ -43,6 +44,18 @@ SIGNATURES = {
     "readme_moe_gate_up_gather": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _P]),
     "readme_moe_down_scatter": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _P]),
     "readme_moe_down": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P]),
+    "readme_packed_experts_permanent_bytes": (_SZ, [_I32, _I32, _I64, _I64, _I64]),
+    "readme_pack_experts_permanent": (_I32, [_I32, _I32, _I64, _I64, _I64, _P, _P, _P, _P, _P,
+                                             _P, _P, _SZ, _P]),
+    "readme_moe_ffn_permanent_workspace_bytes": (_SZ, [_I32, _I64, _I64, _I64]),
+    "readme_moe_ffn_permanent": (_I32, [_I32, _I64, _I64, _I32, _I64, _I64, _P, _P, _P, _P, _P,
+                                        _SZ, _P]),
+    "readme_moe_ffn_permanent_fused": (_I32, [_I32, _I64, _I64, _I32, _I64, _I64, _P, _P, _P,
+                                              _P, _P, _P, _SZ, _P]),
+    "readme_moe_gate_up_permanent_gather": (_I32, [_I32, _I64, _I64, _I32, _I64, _I64, _P, _P,
+                                                   _P, _P, _P, _P]),
+    "readme_moe_down_permanent_scatter": (_I32, [_I32, _I64, _I64, _I32, _I64, _I64, _P, _P, _P,
+                                                 _P, _P, _P]),
     "readme_ungroup": (_I32, [_I32, _I64, _I64, _P, _P, _P, _P]),
     "readme_moe_ffn_stack_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
     "readme_moe_ffn_stack": (_I32, [_I64, _I64, _I32, _I64, _I32, _P, _P, _P, _F, _P,
@@ -247,6 +260,91 @@ def readme_moe_down(h, offsets, packed, E, I, d, y_grouped=None):
     _call("readme_moe_down", _dt(h), T, d, E, I, _p(h), _p(offsets), _p(packed),
           _p(y_grouped), _stream(h.device))
     return y_grouped
+
+
+def readme_packed_experts_permanent_bytes(dtype, E, d, I, P) -> int:
+    return int(load().readme_packed_experts_permanent_bytes(
+        _dt(torch.empty(0, dtype=dtype)), E, d, I, P))
+
+
+def readme_pack_experts_permanent(w_gate, w_up, w_down, p_gate, p_up, p_down, packed=None):
+    """Repack the routed experts ([E][I][d], [E][I][d], [E][d][I]) and the
+    permanent expert ([P][d], [P][d], [d][P]); returns the packed bytes."""
+    E, I, d = w_gate.shape
+    P = p_gate.shape[0]
+    dt = _dt(w_gate)
+    nbytes = readme_packed_experts_permanent_bytes(w_gate.dtype, E, d, I, P)
+    if packed is None:
+        packed = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=w_gate.device)
+    _dev(w_gate, w_up, w_down, p_gate, p_up, p_down, packed)
+    if w_up.shape != w_gate.shape or w_down.shape != (E, d, I):
+        raise ValueError("expert weight shapes disagree")
+    if p_gate.shape != (P, d) or p_up.shape != (P, d) or p_down.shape != (d, P):
+        raise ValueError("permanent expert shapes disagree")
+    if any(t.dtype != w_gate.dtype for t in (w_up, w_down, p_gate, p_up, p_down)):
+        raise ValueError("weight dtypes disagree")
+    _call("readme_pack_experts_permanent", dt, E, d, I, P, _p(w_gate), _p(w_up), _p(w_down),
+          _p(p_gate), _p(p_up), _p(p_down), _p(packed), packed.numel() * packed.element_size(),
+          _stream(w_gate.device))
+    return packed
+
+
+def readme_moe_ffn_permanent_workspace_bytes(dtype, T, I, P) -> int:
+    return int(load().readme_moe_ffn_permanent_workspace_bytes(
+        _dt(torch.empty(0, dtype=dtype)), T, I, P))
+
+
+def readme_moe_ffn_permanent(x_grouped, offsets, packed, E, I, P, y_grouped=None,
+                             workspace=None):
+    """Routed expert + permanent expert on the grouped rows; returns y_grouped."""
+    T, d = x_grouped.shape
+    if y_grouped is None:
+        y_grouped = torch.empty_like(x_grouped)
+    ws = readme_moe_ffn_permanent_workspace_bytes(x_grouped.dtype, T, I, P)
+    if workspace is None:
+        workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=x_grouped.device)
+    _dev(x_grouped, offsets, packed, y_grouped, workspace)
+    _call("readme_moe_ffn_permanent", _dt(x_grouped), T, d, E, I, P, _p(x_grouped),
+          _p(offsets), _p(packed), _p(y_grouped), _p(workspace),
+          workspace.numel() * workspace.element_size(), _stream(x_grouped.device))
+    return y_grouped
+
+
+def readme_moe_ffn_permanent_fused(x, perm, offsets, packed, E, I, P, y=None, workspace=None):
+    """readme_moe_ffn_permanent with the row moves inside the GEMMs; returns y in
+    token order (rows of unrouted tokens are not written)."""
+    T, d = x.shape
+    if y is None:
+        y = torch.empty_like(x)
+    ws = readme_moe_ffn_permanent_workspace_bytes(x.dtype, T, I, P)
+    if workspace is None:
+        workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=x.device)
+    _dev(x, perm, offsets, packed, y, workspace)
+    _call("readme_moe_ffn_permanent_fused", _dt(x), T, d, E, I, P, _p(x), _p(perm), _p(offsets),
+          _p(packed), _p(y), _p(workspace), workspace.numel() * workspace.element_size(),
+          _stream(x.device))
+    return y
+
+
+def readme_moe_gate_up_permanent_gather(x, perm, offsets, packed, E, I, P, h=None):
+    """Gate/up half of readme_moe_ffn_permanent_fused; returns h [T][(1+P/I)*Ip]."""
+    T, d = x.shape
+    if h is None:
+        h = torch.empty(T, (1 + P // I) * readme_padded_intermediate(I), dtype=x.dtype,
+                        device=x.device)
+    _dev(x, perm, offsets, packed, h)
+    _call("readme_moe_gate_up_permanent_gather", _dt(x), T, d, E, I, P, _p(x), _p(perm),
+          _p(offsets), _p(packed), _p(h), _stream(x.device))
+    return h
+
+
+def readme_moe_down_permanent_scatter(h, perm, offsets, packed, E, I, P, d, y):
+    """Down half of readme_moe_ffn_permanent_fused: writes y[perm[j]]."""
+    T = h.shape[0]
+    _dev(h, perm, offsets, packed, y)
+    _call("readme_moe_down_permanent_scatter", _dt(h), T, d, E, I, P, _p(h), _p(perm),
+          _p(offsets), _p(packed), _p(y), _stream(h.device))
+    return y
 
 
 def readme_ungroup(y_grouped, inv_perm, y=None):

@@ -63,6 +63,46 @@ GemmArgs down_args(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I, 
     return g;
 }
 
+// Permanent expert of P neurons, held as P / I slices of one expert's shape.
+inline bool permanent_ok(int64_t P, int64_t I) {
+    return P >= 0 && I >= 1 && P % I == 0 && P / I <= README_MAX_PERMANENT_SLICES;
+}
+
+// The two GEMMs of a layer with a permanent expert of S slices.  h holds
+// [T][(1+S)*Ip]: the routed expert's neurons, then each slice's.  Row maps
+// as in the fused entry points (NULL = grouped rows in and out).
+hipError_t gate_up_permanent(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I,
+                             int64_t S, const void* a, const int32_t* a_rows,
+                             const int32_t* offsets, const void* packed, void* h, hipStream_t s) {
+    GemmArgs gu = gate_up_args(dt, T, d, E, I, a, offsets, packed, h);
+    gu.ldc = (1 + S) * padded_I(I);
+    gu.shared_groups = (int)S;
+    gu.shared_col_stride = padded_I(I);
+    gu.a_rows = a_rows;
+    return launch_grouped_gemm(dt == README_F32, EPI_GATE_UP_SILU, gu, s);
+}
+
+hipError_t down_permanent(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I,
+                          int64_t S, const void* h, const int32_t* offsets, const void* packed,
+                          void* y, const int32_t* c_rows, hipStream_t s) {
+    GemmArgs dn = down_args(dt, T, d, E, I, h, offsets, packed, y);
+    dn.B = reinterpret_cast<const char*>(packed) + packed_gate_up_bytes(dt, E + S, d, I);
+    dn.lda = (1 + S) * padded_I(I);
+    dn.K = (1 + S) * padded_I(I);
+    dn.k_segs = (int)(1 + S);
+    dn.c_rows = c_rows;
+    return launch_grouped_gemm(dt == README_F32, EPI_STORE, dn, s);
+}
+
+readme_status ffn_permanent(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I,
+                            int64_t S, const void* a, const int32_t* a_rows,
+                            const int32_t* offsets, const void* packed, void* y,
+                            const int32_t* c_rows, void* h, hipStream_t s) {
+    hipError_t err = gate_up_permanent(dt, T, d, E, I, S, a, a_rows, offsets, packed, h, s);
+    if (err == hipSuccess) err = down_permanent(dt, T, d, E, I, S, h, offsets, packed, y, c_rows, s);
+    return hip_status(err);
+}
+
 }  // namespace
 
 extern "C" {
@@ -222,6 +262,104 @@ readme_status readme_moe_ffn_fused(readme_dtype dt, int64_t T, int64_t d, int32_
     st = readme_moe_gate_up_gather(dt, T, d, E, I, x, perm, offsets, packed, workspace, stream);
     if (st != README_OK) return st;
     return readme_moe_down_scatter(dt, T, d, E, I, workspace, perm, offsets, packed, y, stream);
+}
+
+size_t readme_packed_experts_permanent_bytes(readme_dtype dt, int32_t E, int64_t d, int64_t I,
+                                             int64_t P) {
+    if (!dtype_ok(dt) || !experts_ok(E) || d <= 0 || !permanent_ok(P, I)) return 0;
+    return packed_bytes(dt, E + P / I, d, I);
+}
+
+readme_status readme_pack_experts_permanent(readme_dtype dt, int32_t E, int64_t d, int64_t I,
+                                            int64_t P, const void* w_gate, const void* w_up,
+                                            const void* w_down, const void* p_gate,
+                                            const void* p_up, const void* p_down, void* packed,
+                                            size_t packed_bytes_given, void* stream) {
+    readme_status st = check_ffn_shape(dt, 0, d, E, I);
+    if (st != README_OK) return st;
+    if (!permanent_ok(P, I)) return P < 0 ? README_ERR_ARG : README_ERR_UNSUPPORTED;
+    const int64_t S = P / I;
+    if (!w_gate || !w_up || !w_down || !packed) return README_ERR_ARG;
+    if (S > 0 && (!p_gate || !p_up || !p_down)) return README_ERR_ARG;
+    if (!a16(packed)) return README_ERR_ARG;
+    if (packed_bytes_given < packed_bytes(dt, E + S, d, I)) return README_ERR_WORKSPACE;
+    hipStream_t s = as_stream(stream);
+    hipError_t err = launch_pack_slots(dt, E + S, 0, E, d, I, w_gate, w_up, w_down, d * I, I,
+                                       packed, s);
+    // Slice j of the permanent expert: rows j*I .. of p_gate/p_up, columns
+    // j*I .. of p_down (row stride P).
+    if (err == hipSuccess && S > 0)
+        err = launch_pack_slots(dt, E + S, E, S, d, I, p_gate, p_up, p_down, I, P, packed, s);
+    return hip_status(err);
+}
+
+size_t readme_moe_ffn_permanent_workspace_bytes(readme_dtype dt, int64_t T, int64_t I,
+                                                int64_t P) {
+    if (!dtype_ok(dt) || T < 0 || !permanent_ok(P, I)) return 0;
+    return (size_t)T * (1 + P / I) * padded_I(I) * dtype_size(dt);
+}
+
+readme_status readme_moe_ffn_permanent(readme_dtype dt, int64_t T, int64_t d, int32_t E,
+                                       int64_t I, int64_t P, const void* x_grouped,
+                                       const int32_t* offsets, const void* packed,
+                                       void* y_grouped, void* workspace, size_t workspace_bytes,
+                                       void* stream) {
+    readme_status st = check_ffn_shape(dt, T, d, E, I);
+    if (st != README_OK) return st;
+    if (!permanent_ok(P, I)) return P < 0 ? README_ERR_ARG : README_ERR_UNSUPPORTED;
+    if (T == 0) return README_OK;
+    if (!x_grouped || !offsets || !packed || !y_grouped || !workspace) return README_ERR_ARG;
+    if (!a16(x_grouped) || !a16(packed) || !a16(y_grouped) || !a16(workspace))
+        return README_ERR_ARG;
+    if (workspace_bytes < readme_moe_ffn_permanent_workspace_bytes(dt, T, I, P))
+        return README_ERR_WORKSPACE;
+    return ffn_permanent(dt, T, d, E, I, P / I, x_grouped, nullptr, offsets, packed, y_grouped,
+                         nullptr, workspace, as_stream(stream));
+}
+
+readme_status readme_moe_ffn_permanent_fused(readme_dtype dt, int64_t T, int64_t d, int32_t E,
+                                             int64_t I, int64_t P, const void* x,
+                                             const int32_t* perm, const int32_t* offsets,
+                                             const void* packed, void* y, void* workspace,
+                                             size_t workspace_bytes, void* stream) {
+    readme_status st = check_ffn_shape(dt, T, d, E, I);
+    if (st != README_OK) return st;
+    if (!permanent_ok(P, I)) return P < 0 ? README_ERR_ARG : README_ERR_UNSUPPORTED;
+    if (T == 0) return README_OK;
+    if (!x || !perm || !offsets || !packed || !y || !workspace) return README_ERR_ARG;
+    if (!a16(x) || !a16(packed) || !a16(y) || !a16(workspace)) return README_ERR_ARG;
+    if (workspace_bytes < readme_moe_ffn_permanent_workspace_bytes(dt, T, I, P))
+        return README_ERR_WORKSPACE;
+    return ffn_permanent(dt, T, d, E, I, P / I, x, perm, offsets, packed, y, perm, workspace,
+                         as_stream(stream));
+}
+
+readme_status readme_moe_gate_up_permanent_gather(readme_dtype dt, int64_t T, int64_t d,
+                                                  int32_t E, int64_t I, int64_t P, const void* x,
+                                                  const int32_t* perm, const int32_t* offsets,
+                                                  const void* packed, void* h, void* stream) {
+    readme_status st = check_ffn_shape(dt, T, d, E, I);
+    if (st != README_OK) return st;
+    if (!permanent_ok(P, I)) return P < 0 ? README_ERR_ARG : README_ERR_UNSUPPORTED;
+    if (T == 0) return README_OK;
+    if (!x || !perm || !offsets || !packed || !h) return README_ERR_ARG;
+    if (!a16(x) || !a16(packed) || !a16(h)) return README_ERR_ARG;
+    return hip_status(gate_up_permanent(dt, T, d, E, I, P / I, x, perm, offsets, packed, h,
+                                        as_stream(stream)));
+}
+
+readme_status readme_moe_down_permanent_scatter(readme_dtype dt, int64_t T, int64_t d, int32_t E,
+                                                int64_t I, int64_t P, const void* h,
+                                                const int32_t* perm, const int32_t* offsets,
+                                                const void* packed, void* y, void* stream) {
+    readme_status st = check_ffn_shape(dt, T, d, E, I);
+    if (st != README_OK) return st;
+    if (!permanent_ok(P, I)) return P < 0 ? README_ERR_ARG : README_ERR_UNSUPPORTED;
+    if (T == 0) return README_OK;
+    if (!h || !perm || !offsets || !packed || !y) return README_ERR_ARG;
+    if (!a16(h) || !a16(packed) || !a16(y)) return README_ERR_ARG;
+    return hip_status(down_permanent(dt, T, d, E, I, P / I, h, offsets, packed, y, perm,
+                                     as_stream(stream)));
 }
 
 readme_status readme_ungroup(readme_dtype dt, int64_t T, int64_t d, const void* y_grouped,

@@ -1,5 +1,7 @@
 // Host side of the grouped GEMM: tile choice and dispatch.  The kernels are
 // in gemm_kernels.hpp, instantiated in gemm_f32.hip and gemm_bf16_*.hip.
+#include <limits.h>
+
 #include "gemm_kernels.hpp"
 
 namespace readme {
@@ -30,6 +32,12 @@ static int tile_by_shape(bool gate_up, const GemmArgs& g) {
 }
 
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s) {
+    // The kernels address one weight index with 32-bit per-lane offsets and
+    // find a K-step's segment by a multiply-high that is exact below 2^16
+    // K-steps (K-steps are at least 32 elements).
+    if (g.b_expert_stride * (f32 ? 4 : 2) > INT32_MAX) return hipErrorInvalidValue;
+    if (g.K >= (int64_t)32 << 16) return hipErrorInvalidValue;
+    if (g.k_segs > 1 && epi != EPI_STORE) return hipErrorInvalidValue;  // segments: down only
     const int tile = tile_by_shape(epi == EPI_GATE_UP_SILU, g);
     if (f32) {
         if (epi == EPI_GATE_UP_SILU) return launch_tile_f32_gate_up(tile, g, s);

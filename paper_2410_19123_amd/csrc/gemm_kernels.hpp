@@ -154,11 +154,15 @@ __device__ __forceinline__ int wave_incl_scan(int v, int lane) {
     return v;
 }
 
-// Rows [s, en) of expert ee, offsets clamped to [0, T] (a corrupt offsets
+// Rows [s, en) of row group ee, offsets clamped to [0, T] (a corrupt offsets
 // array cannot make a tile leave the rows); returns its M tiles of size BM.
+// Groups 0 .. E-1 are the experts; a permanent-expert group (ee >= E) covers
+// every routed row.
 template <int BM>
 __device__ __forceinline__ int expert_rows(const GemmArgs& g, int ee, int& s, int& en) {
-    int64_t a = g.offsets[ee], b = g.offsets[ee + 1];
+    const int i0 = ee < g.E ? ee : g.E - 1;  // one adjacent pair of offsets
+    int64_t a = g.offsets[i0], b = g.offsets[i0 + 1];
+    if (ee >= g.E) a = 0;
     a = a < 0 ? 0 : (a > g.T ? g.T : a);
     b = b < a ? a : (b > g.T ? g.T : b);
     s = (int)a;
@@ -166,15 +170,19 @@ __device__ __forceinline__ int expert_rows(const GemmArgs& g, int ee, int& s, in
     return (int)((b - a + BM - 1) / BM);
 }
 
-// Number of BM-row tiles over all experts (times g.n_tiles N tiles), read
-// from the device offsets 64 experts at a time; wave-uniform.
+// Row groups: the E experts, then the permanent expert's groups.
+__device__ __forceinline__ int row_groups(const GemmArgs& g) { return g.E + g.shared_groups; }
+
+// Number of BM-row tiles over all row groups (times g.n_tiles N tiles), read
+// from the device offsets 64 groups at a time; wave-uniform.
 template <int BM>
 __device__ __forceinline__ int count_tiles(const GemmArgs& g) {
     const int lane = threadIdx.x & 63;
+    const int G = row_groups(g);
     int total = 0;
-    for (int c0 = 0; c0 < g.E; c0 += 64) {
+    for (int c0 = 0; c0 < G; c0 += 64) {
         int s = 0, en = 0, tiles = 0;
-        if (c0 + lane < g.E) tiles = expert_rows<BM>(g, c0 + lane, s, en) * g.n_tiles;
+        if (c0 + lane < G) tiles = expert_rows<BM>(g, c0 + lane, s, en) * g.n_tiles;
         total += __shfl(wave_incl_scan(tiles, lane), 63, 64);
     }
     return __builtin_amdgcn_readfirstlane(total);
@@ -188,16 +196,17 @@ template <int BM, int BMG>
 __device__ __forceinline__ bool locate_tile(const GemmArgs& g, int L, TileLoc& t) {
     const int lane = threadIdx.x & 63;
     const int nt_n = g.n_tiles;
+    const int G = row_groups(g);
     int base = 0, gbase = 0;
-    for (int c0 = 0; c0 < g.E; c0 += 64) {
+    for (int c0 = 0; c0 < G; c0 += 64) {
         int s = 0, en = 0, mt_e = 0, mg_e = 0;
-        if (c0 + lane < g.E) {
+        if (c0 + lane < G) {
             mt_e = expert_rows<BM>(g, c0 + lane, s, en);
             mg_e = (en - s + BMG - 1) / BMG;
         }
         const int incl = wave_incl_scan(mt_e * nt_n, lane) + base;
         const int gincl = wave_incl_scan(mg_e, lane) + gbase;
-        const uint64_t hit = __ballot(c0 + lane < g.E && L < incl);
+        const uint64_t hit = __ballot(c0 + lane < G && L < incl);
         if (hit) {
             const int src = __builtin_ctzll(hit);
             const int e_s = __builtin_amdgcn_readfirstlane(__shfl(s, src, 64));
@@ -244,6 +253,55 @@ __device__ __forceinline__ bool find_tile(const GemmArgs& g, TileLoc& t) {
     return locate_tile<BM, BM>(g, L, t);
 }
 
+// The arguments one tile works with: a permanent-expert row group writes
+// its own block of output columns.
+template <typename OT>
+__device__ __forceinline__ GemmArgs tile_args(const GemmArgs& g, int e) {
+    GemmArgs a = g;
+    if (e >= g.E)
+        a.C = reinterpret_cast<OT*>(g.C) + (int64_t)(e - g.E + 1) * g.shared_col_stride;
+    return a;
+}
+
+// Weights of the K-steps of one tile.  The per-lane part of an address (row
+// group, fragment, lane) is the same in every K segment; the segment's base
+// and the step within it are wave-uniform.  Segment 0 is the tile's own
+// weights (index e), segment s >= 1 the permanent slice of index E+s-1.
+struct WeightSteps {
+    const char* own;     // index e
+    const char* B0;      // index 0
+    int64_t estride;     // bytes per weight index
+    int64_t step_bytes;  // bytes per K-step of one row group
+    uint32_t nks;        // K-steps per segment
+    uint32_t mult;       // ceil(2^32 / nks) with several segments, else 0
+    int E;
+
+    // Segment of K-step kt = floor(kt * mult / 2^32), exact for kt and nks
+    // below 2^16 (the launcher checks K); 0 throughout with one segment.
+    __device__ __forceinline__ const char* at(int kt) const {
+        const uint32_t sg = __umulhi((uint32_t)kt, mult);
+        const char* base = sg == 0 ? own : B0 + (int64_t)(E + (int)sg - 1) * estride;
+        return base + (int64_t)(kt - (int)(sg * nks)) * step_bytes;
+    }
+};
+
+// SEG: the kernel may run K segments (the down projection of a layer with a
+// permanent expert); otherwise the segment is 0 at compile time.
+template <bool SEG>
+__device__ __forceinline__ WeightSteps weight_steps(const GemmArgs& g, int e, int esz,
+                                                    int64_t bk, int64_t step_bytes) {
+    WeightSteps w;
+    const int segs = SEG && g.k_segs > 1 ? g.k_segs : 1;
+    w.B0 = reinterpret_cast<const char*>(g.B);
+    w.estride = g.b_expert_stride * esz;
+    w.own = w.B0 + (int64_t)e * w.estride;
+    w.step_bytes = step_bytes;
+    w.nks = (uint32_t)(g.K / segs / bk);
+    w.mult = segs > 1 ? (uint32_t)(((1ull << 32) + w.nks - 1) / w.nks) : 0u;
+    w.E = g.E;
+    return w;
+}
+
 // Residual epilogue (stacked layers, no row maps): the fp32 residual values
 // a wave will update are loaded into its accumulators before the K loop, so
 // the epilogue does not wait on them and stores the sum.  Each element
@@ -265,50 +323,6 @@ __device__ __forceinline__ void load_residual(const GemmArgs& g, f32x16 (&acc)[T
                 acc[i][j][r] = res[grow * g.ldc + c];
             }
         }
-}
-
-// Epilogue of a wave's TM x TN block of 32x32 tiles whose first row is tile
-// row row0 and first column col0.  Accumulator layout of a 32x32 tile:
-// register r of lane l holds row 8*(r/4) + 4*(l/32) + r%4, column l%32.
-template <int TM, int TN, bool F32, int EPI>
-__device__ __forceinline__ void store_tile(const GemmArgs& g, const f32x16 (&acc)[TM][TN],
-                                           int row0, int64_t col0, int rows, int64_t m0,
-                                           const int32_t* crow, int lane) {
-    const int col = lane & 31;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int rt = row0 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            if (rt >= rows) continue;
-            const int64_t grow = g.c_rows ? (int64_t)crow[rt] : m0 + rt;
-            if (grow < 0 || grow >= g.T) continue;  // a corrupt map writes nothing
-            if constexpr (EPI == EPI_GATE_UP_SILU) {
-#pragma unroll
-                for (int j = 0; j < TN; j += 2) {
-                    const int64_t nb0 = col0 + j * 32;  // gate group start
-                    if (nb0 >= g.N) continue;
-                    const float h = silu_f32(acc[i][j][r]) * acc[i][j + 1][r];
-                    const int64_t hc = nb0 / 2 + col;
-                    if constexpr (F32)
-                        reinterpret_cast<float*>(g.C)[grow * g.ldc + hc] = h;
-                    else
-                        reinterpret_cast<uint16_t*>(g.C)[grow * g.ldc + hc] = f32_to_bf16(h);
-                }
-            } else {
-#pragma unroll
-                for (int j = 0; j < TN; ++j) {
-                    if (col0 + j * 32 >= g.N) continue;
-                    const int64_t c = col0 + j * 32 + col;
-                    const float v = acc[i][j][r];
-                    if constexpr (EPI == EPI_RESID_ADD || F32)
-                        reinterpret_cast<float*>(g.C)[grow * g.ldc + c] = v;
-                    else
-                        reinterpret_cast<uint16_t*>(g.C)[grow * g.ldc + c] = f32_to_bf16(v);
-                }
-            }
-        }
-    }
 }
 
 // Epilogue through LDS.  The accumulator layout gives each lane one column
@@ -391,7 +405,7 @@ struct Epilogue {
 };
 
 template <int BM, int BN, int WGM, int WGN, int NSTAGE, bool F32, int EPI, int KC = CPR>
-__global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
+__global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs args) {
     constexpr int NW = WGM * WGN;
     constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int TM = WM / 32, TN = WN / 32;
@@ -426,7 +440,8 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     const int wm = wave / WGN, wn = wave % WGN;
 
     TileLoc t;
-    if (!find_tile<BM>(g, t)) return;
+    if (!find_tile<BM>(args, t)) return;
+    const GemmArgs g = tile_args<typename Epi::OT>(args, t.e);
     const int e = t.e;
     const int64_t m0 = t.m0, m_end = t.m_end;
     const int rows = t.rows;
@@ -458,26 +473,26 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs g) {
     // KC/2 KB of each group's stream: KB q of the stage's B region is KB
     // q % (KC/2) of group q / (KC/2).  N tiles past the last group reuse it
     // (their columns are never stored).
-    const char* Bb = reinterpret_cast<const char*>(g.B) + (int64_t)e * g.b_expert_stride * ESZ;
-    const int64_t group_bytes = (g.K / (CPR * EPC)) * 4096;
-    const char* b_src[B_INS];
+    const WeightSteps wst = weight_steps<EPI == EPI_STORE>(g, e, ESZ, BK, KC * 512);
+    const int64_t group_bytes = (int64_t)wst.nks * KC * 512;  // per K segment
+    uint32_t b_off[B_INS];
 #pragma unroll
     for (int i = 0; i < B_INS; ++i) {
         const int q = wave + NW * i;
         int64_t grp = (n0 >> 5) + q / (KC / 2);
         const int64_t last = (g.N >> 5) - 1;
         grp = grp < last ? grp : last;
-        b_src[i] = Bb + grp * group_bytes + (q % (KC / 2)) * 1024 + lane * 16;
+        b_off[i] = (uint32_t)(grp * group_bytes + (q % (KC / 2)) * 1024 + lane * 16);
     }
 
     auto issue = [&](int stage, int kt) {
         u32x4* base = lds + stage * STAGE;
         const int64_t aoff = (int64_t)kt * KC * 16;
-        const int64_t boff = (int64_t)kt * KC * 512;
+        const char* bs = wst.at(kt);
 #pragma unroll
         for (int i = 0; i < A_INS; ++i) dma16(a_src[i] + aoff, base + (wave + NW * i) * 64);
 #pragma unroll
-        for (int i = 0; i < B_INS; ++i) dma16(b_src[i] + boff, base + BM * KC + (wave + NW * i) * 64);
+        for (int i = 0; i < B_INS; ++i) dma16(bs + b_off[i], base + BM * KC + (wave + NW * i) * 64);
     };
 
     // Output rows of this tile, staged once: the epilogue then needs no
@@ -618,28 +633,27 @@ struct BdTile {
 
     // Weight fragments of this wave: row group (col0/32 + j), clamped to the
     // last group for columns past N (loaded, never stored).
-    const int64_t ksteps = g.K / BK;
-    const char* Bb = reinterpret_cast<const char*>(g.B) + (int64_t)t.e * g.b_expert_stride * ESZ;
-    const char* b_src[TN];
+    const int nk = (int)(g.K / BK);
+    const WeightSteps wst = weight_steps<EPI == EPI_STORE>(g, t.e, ESZ, BK, 4096);
+    uint32_t b_off[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         int64_t grp = (col0 >> 5) + j;
         const int64_t last = (g.N >> 5) - 1;
         grp = grp < last ? grp : last;
-        b_src[j] = Bb + grp * ksteps * 4096 + lane * 16;
+        b_off[j] = (uint32_t)(grp * wst.nks * 4096 + lane * 16);
     }
 
-    const int nk = (int)ksteps;
     u32x4 bq[S][TN][CPR / 2];
     auto load_b = [&](auto sc, int kt) {
         constexpr int sl = decltype(sc)::value;
         kt = kt < nk ? kt : nk - 1;
+        const char* bs = wst.at(kt);
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
             for (int q = 0; q < CPR / 2; ++q)
-                bq[sl][j][q] =
-                    *reinterpret_cast<const u32x4*>(b_src[j] + (int64_t)kt * 4096 + q * 1024);
+                bq[sl][j][q] = *reinterpret_cast<const u32x4*>(bs + b_off[j] + q * 1024);
     };
     // The weight stream does not depend on the row map: its first K-steps
     // are requested before the row map is read.
@@ -712,12 +726,12 @@ struct BdTile {
     // registers, spread over the step, so the address unit streams while the
     // matrix cores work instead of taking every load at the end of the step.
     constexpr int KK = CPR / 2;
-    auto refill = [&](auto sc, int kt, int kk) {
+    // kt is already clamped and bs = wst.at(kt), both once per K-step.
+    auto refill = [&](auto sc, const char* bs, int kt, int kk) {
         constexpr int sl = decltype(sc)::value;
-        kt = kt < nk ? kt : nk - 1;
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-            bq[sl][j][kk] = *reinterpret_cast<const u32x4*>(b_src[j] + (int64_t)kt * 4096 + kk * 1024);
+            bq[sl][j][kk] = *reinterpret_cast<const u32x4*>(bs + b_off[j] + kk * 1024);
 #pragma unroll
         for (int i = kk * A_INS / KK; i < (kk + 1) * A_INS / KK; ++i)
             aq[sl][i] = *reinterpret_cast<const u32x4*>(a_src[i] + (int64_t)kt * 128);
@@ -725,6 +739,8 @@ struct BdTile {
     auto step = [&](auto sc, int kt) {
         constexpr int s = decltype(sc)::value;
         const u32x4* L = lds + (kt & 1) * STAGE;
+        const int ktn = kt + S < nk ? kt + S : nk - 1;  // K-step the refills fetch
+        const char* bsn = wst.at(ktn);
         u32x4 af[2][TM];
         auto frag = [&](int buf, int kk) {
             const int ch = swz(2 * kk + fhalf, frow);
@@ -752,7 +768,7 @@ struct BdTile {
                             __builtin_bit_cast(bf16x8, bq[s][j][kk]), acc[i][j], 0, 0, 0);
                     }
                 }
-            refill(sc, kt + S, kk);
+            refill(sc, bsn, ktn, kk);
         }
         sched_bd_step<TM * TN * (F32 ? 4 : 1), TM, TN + A_INS / KK, KK>();
         store_a(std::integral_constant<int, (s + 1) % S>{}, (kt + 1) & 1);
@@ -777,16 +793,23 @@ __global__ __launch_bounds__(NW * 64) void k_grouped_gemm_bd(GemmArgs g) {
     __shared__ int32_t crow[BM];
     TileLoc t;
     if (!find_tile<BM>(g, t)) return;
-    Tile::run(g, t, lds, crow);
+    Tile::run(tile_args<typename Tile::Epi::OT>(g, t.e), t, lds, crow);
+}
+
+// Upper bound of the M tiles over all row groups: sum_e ceil(T_e / BM) <=
+// (T + E*(BM-1)) / BM (and <= T) for the experts, ceil(T / BM) per
+// permanent-expert group.
+inline int64_t m_tiles_bound(const GemmArgs& g, int BM) {
+    int64_t mt = (g.T + (int64_t)g.E * (BM - 1)) / BM;
+    if (mt > g.T) mt = g.T;
+    return mt + (int64_t)g.shared_groups * ceil_div(g.T, (int64_t)BM);
 }
 
 template <int BM, int NW, int TN, int SA, bool F32, int EPI>
 inline hipError_t launch_bd(GemmArgs g, hipStream_t s) {
     constexpr int BN = NW * TN * 32;
     g.n_tiles = (int)ceil_div(g.N, BN);
-    int64_t mt = (g.T + (int64_t)g.E * (BM - 1)) / BM;
-    if (mt > g.T) mt = g.T;
-    g.m_tiles_max = (int)mt;
+    g.m_tiles_max = (int)m_tiles_bound(g, BM);
     const int64_t blocks = round_up((int64_t)g.n_tiles * g.m_tiles_max, 8);
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
@@ -797,9 +820,7 @@ inline hipError_t launch_bd(GemmArgs g, hipStream_t s) {
 template <int BM, int BN, int WGM, int WGN, int NSTAGE, bool F32, int EPI, int KC = CPR>
 inline hipError_t launch_cfg(GemmArgs g, hipStream_t s) {
     g.n_tiles = (int)ceil_div(g.N, BN);
-    int64_t mt = (g.T + (int64_t)g.E * (BM - 1)) / BM;
-    if (mt > g.T) mt = g.T;
-    g.m_tiles_max = (int)mt;
+    g.m_tiles_max = (int)m_tiles_bound(g, BM);
     const int64_t blocks = round_up((int64_t)g.n_tiles * g.m_tiles_max, 8);
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;

@@ -27,6 +27,17 @@ struct GemmArgs {
     // a_rows[j]; output row j is written to C row c_rows[j].  NULL = identity.
     const int32_t* a_rows;
     const int32_t* c_rows;
+    // Permanent expert (neurons every routed token passes through), stored
+    // as slices of one expert's shape at weight indices E, E+1, ...:
+    //   shared_groups S > 0 (gate/up): S more row groups after the E experts,
+    //     group E+i covering every routed row [0, offsets[E]) with the
+    //     weights of index E+i and its output columns shifted right by
+    //     (i+1) * shared_col_stride;
+    //   k_segs > 1 (down): K is k_segs equal segments; segment 0 multiplies
+    //     the expert's own weights, segment s >= 1 those of index E+s-1.
+    int shared_groups;
+    int64_t shared_col_stride;  // elements
+    int k_segs;
     int n_tiles, m_tiles_max; // filled by the launcher
 };
 
@@ -39,6 +50,13 @@ hipError_t launch_move_rows(int64_t nrows, int64_t row_bytes, const void* src, c
                             int64_t src_rows, void* dst, hipStream_t s);
 hipError_t launch_pack(readme_dtype dt, int64_t E, int64_t d, int64_t I, const void* wg,
                        const void* wu, const void* wd, void* packed, hipStream_t s);
+// Packs n experts into slots e0 .. e0+n-1 of a packed buffer of E_all slots.
+// Expert j's gate/up rows at wg/wu + j * I * d (row stride d); its down
+// element (c, i) at wd[j * wd_expert_stride + c * wd_row_stride + i].
+hipError_t launch_pack_slots(readme_dtype dt, int64_t E_all, int64_t e0, int64_t n, int64_t d,
+                             int64_t I, const void* wg, const void* wu, const void* wd,
+                             int64_t wd_expert_stride, int64_t wd_row_stride, void* packed,
+                             hipStream_t s);
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s);
 bool set_gemm_tile(int tile);
 hipError_t launch_rms_to_bf16(int64_t T, int64_t d, const float* x, const int32_t* offsets, int E,

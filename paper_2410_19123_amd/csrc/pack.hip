@@ -56,9 +56,11 @@ __global__ __launch_bounds__(256) void k_pack_gate_up(int64_t E, int64_t d, int6
     }
 }
 
-// Down: destination element of [d][Ip] (logical) from W_down [E][d][I].
+// Down: destination element of [d][Ip] (logical) from W_down, expert e's
+// element (c, i) at wd[e * es + c * rs + i] ([E][d][I]: es = d*I, rs = I).
 template <typename T>
 __global__ __launch_bounds__(256) void k_pack_down(int64_t E, int64_t d, int64_t I, int64_t Ip,
+                                                   int64_t es, int64_t rs,
                                                    const T* __restrict__ wd,
                                                    char* __restrict__ out) {
     const int64_t per_e = d * Ip;
@@ -69,29 +71,42 @@ __global__ __launch_bounds__(256) void k_pack_down(int64_t E, int64_t d, int64_t
         const int64_t e = o / per_e;
         const int64_t rem = o - e * per_e;
         const int64_t c = rem / Ip, i = rem % Ip;
-        const T v = i < I ? wd[(e * d + c) * I + i] : T(0);
+        const T v = i < I ? wd[e * es + c * rs + i] : T(0);
         *reinterpret_cast<T*>(out + e * per_e * (int64_t)sizeof(T) +
                               blocked_offset(c, i, ksteps, sizeof(T))) = v;
     }
 }
 
 template <typename T>
-static hipError_t pack_t(int64_t E, int64_t d, int64_t I, const void* wg, const void* wu,
-                         const void* wd, void* packed, hipStream_t s) {
+static hipError_t pack_t(int64_t E_all, int64_t e0, int64_t n, int64_t d, int64_t I,
+                         const void* wg, const void* wu, const void* wd, int64_t es, int64_t rs,
+                         void* packed, hipStream_t s) {
     const int64_t Ip = padded_I(I);
-    char* gu = reinterpret_cast<char*>(packed);
-    char* dn = gu + E * 2 * Ip * d * (int64_t)sizeof(T);
+    const int64_t gu_e = 2 * Ip * d * (int64_t)sizeof(T), dn_e = d * Ip * (int64_t)sizeof(T);
+    char* gu = reinterpret_cast<char*>(packed) + e0 * gu_e;
+    char* dn = reinterpret_cast<char*>(packed) + E_all * gu_e + e0 * dn_e;
     const unsigned blocks = 4096;
-    k_pack_gate_up<T><<<blocks, 256, 0, s>>>(E, d, I, Ip, reinterpret_cast<const T*>(wg),
+    k_pack_gate_up<T><<<blocks, 256, 0, s>>>(n, d, I, Ip, reinterpret_cast<const T*>(wg),
                                               reinterpret_cast<const T*>(wu), gu);
-    k_pack_down<T><<<blocks, 256, 0, s>>>(E, d, I, Ip, reinterpret_cast<const T*>(wd), dn);
+    k_pack_down<T><<<blocks, 256, 0, s>>>(n, d, I, Ip, es, rs, reinterpret_cast<const T*>(wd),
+                                           dn);
     return hipGetLastError();
+}
+
+hipError_t launch_pack_slots(readme_dtype dt, int64_t E_all, int64_t e0, int64_t n, int64_t d,
+                             int64_t I, const void* wg, const void* wu, const void* wd,
+                             int64_t wd_expert_stride, int64_t wd_row_stride, void* packed,
+                             hipStream_t s) {
+    if (dt == README_F32)
+        return pack_t<uint32_t>(E_all, e0, n, d, I, wg, wu, wd, wd_expert_stride, wd_row_stride,
+                                packed, s);
+    return pack_t<uint16_t>(E_all, e0, n, d, I, wg, wu, wd, wd_expert_stride, wd_row_stride,
+                            packed, s);
 }
 
 hipError_t launch_pack(readme_dtype dt, int64_t E, int64_t d, int64_t I, const void* wg,
                        const void* wu, const void* wd, void* packed, hipStream_t s) {
-    if (dt == README_F32) return pack_t<uint32_t>(E, d, I, wg, wu, wd, packed, s);
-    return pack_t<uint16_t>(E, d, I, wg, wu, wd, packed, s);
+    return launch_pack_slots(dt, E, 0, E, d, I, wg, wu, wd, d * I, I, packed, s);
 }
 
 }  // namespace readme

@@ -101,3 +101,29 @@ def test_ffn_argument_errors(lib):
     assert s(64, 4096, 8, 1376, 1, arr, FAKE, FAKE, ctypes.c_float(1e-5), FAKE, 10, None) == 3
     assert s(64, 4096, 8, 1376, -1, arr, FAKE, FAKE, ctypes.c_float(1e-5), FAKE, 1 << 40,
              None) == 1
+
+
+def test_permanent_sizes_and_errors(lib):
+    # S = P / I slices of one expert's packed shape after the E experts.
+    assert lib.readme_packed_experts_permanent_bytes(1, 8, 4096, 1376, 1376) == \
+        9 * 3 * 1408 * 4096 * 2
+    assert lib.readme_packed_experts_permanent_bytes(1, 8, 4096, 1376, 0) == \
+        lib.readme_packed_experts_bytes(1, 8, 4096, 1376)
+    assert lib.readme_packed_experts_permanent_bytes(1, 8, 4096, 1376, 1000) == 0  # P % I
+    assert lib.readme_packed_experts_permanent_bytes(1, 8, 4096, 16, 17 * 16) == 0  # > 16 slices
+    assert lib.readme_moe_ffn_permanent_workspace_bytes(1, 2048, 1376, 2752) == \
+        2048 * 3 * 1408 * 2
+    f = lib.readme_moe_ffn_permanent_fused
+    big = 1 << 40
+    assert f(1, 16, 4096, 8, 1376, 1376, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 10, None) == 3
+    assert f(1, 16, 4096, 8, 1376, 1000, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, big, None) == 2
+    assert f(1, 16, 4096, 8, 1376, -1376, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, big, None) == 1
+    assert f(1, 16, 4096, 8, 1376, 1376, FAKE, None, FAKE, FAKE, FAKE, FAKE, big, None) == 1
+    assert f(1, 0, 4096, 8, 1376, 1376, None, None, None, None, None, None, 0, None) == 0
+    g = lib.readme_moe_ffn_permanent
+    assert g(1, 16, 4096, 8, 1376, 1376, FAKE, FAKE, FAKE, FAKE, FAKE, 10, None) == 3
+    assert g(1, 16, 4000, 8, 1376, 1376, FAKE, FAKE, FAKE, FAKE, FAKE, big, None) == 2
+    p = lib.readme_pack_experts_permanent
+    assert p(1, 8, 4096, 1376, 1376, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 100, None) == 3
+    assert p(1, 8, 4096, 1376, 1376, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, big, None) == 1
+    assert p(1, 8, 4096, 1376, 1000, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, big, None) == 2

@@ -1,0 +1,125 @@
+"""Parity of the permanent-expert layer (Sec. 3: neurons every token
+activates, beside its routed expert) on the HIP path, through the C ABI,
+with the CPU oracle.  FFN outputs meet the tolerance in tests/_util.py; the
+row moves, the fused form and the P = 0 case are compared bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2410_19123_amd import workloads as wl
+
+from . import _util as U
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    from paper_2410_19123_amd import _lib
+    _lib.load()
+    return _lib
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _pack(L, w, seed):
+    return L.readme_pack_experts_permanent(
+        *U.weights_to_dev(*wl.make_experts(w, seed)),
+        *U.weights_to_dev(*wl.make_permanent(w, seed)))
+
+
+@pytest.mark.parametrize("tile", list(range(0, 21)))
+def test_every_tile_with_permanent_expert(L, oracle_mod, tile):
+    """Each GEMM tile configuration: the permanent slices as extra row
+    groups over every routed row (gate/up) and as extra K segments (down),
+    on ragged blocks (empty, single-row, tile +- 1, multi-tile experts)."""
+    _say("permanent tile", tile)
+    L.readme_set_gemm_tile(tile)
+    try:
+        for dtype, d, I, P, counts in [("bf16", 256, 200, 400, [0, 1, 255, 257, 33, 520]),
+                                       ("f32", 128, 96, 96, [3, 0, 129, 64])]:
+            E, T = len(counts), sum(counts)
+            w = wl.Workload("t", T=T, d=d, E=E, I=I, P=P, dtype=dtype)
+            x = wl.make_x(w, 20 + tile)
+            offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+            packed = _pack(L, w, 20 + tile)
+            y = L.readme_moe_ffn_permanent(U.to_dev(x), U.to_dev(offsets), packed, E, I, P)
+            torch.cuda.synchronize()
+            ref = oracle_mod.moe_ffn_permanent(x, offsets, *wl.make_experts(w, 20 + tile),
+                                               *wl.make_permanent(w, 20 + tile))
+            U.close(U.from_dev(y), ref, f"tile {tile} {dtype}")
+    finally:
+        L.readme_set_gemm_tile(0)
+
+
+def test_permanent_workload_full_path(L, oracle_mod):
+    """route -> group -> fused permanent-expert FFN at the full workload size,
+    checked on sampled rows of every expert block; the unfused form equals
+    the fused one bit for bit."""
+    w = wl.WORKLOADS["llama7b_layer_perm"]
+    _say("permanent full path", w.name)
+    x = wl.make_x(w)
+    wr, b = wl.make_router(w)
+    xd = U.to_dev(x)
+    ids, _ = L.readme_route(xd, U.to_dev(wr), U.to_dev(b))
+    counts, offs, perm, inv, xg = L.readme_group_by_expert(ids, w.E, x=xd)
+    packed = _pack(L, w, 0)
+    y = L.readme_moe_ffn_permanent_fused(xd, perm, offs, packed, w.E, w.I, w.P)
+    yg = L.readme_moe_ffn_permanent(xg, offs, packed, w.E, w.I, w.P)
+    h = L.readme_moe_gate_up_permanent_gather(xd, perm, offs, packed, w.E, w.I, w.P)
+    y2 = L.readme_moe_down_permanent_scatter(h, perm, offs, packed, w.E, w.I, w.P, w.d,
+                                             torch.empty_like(xd))
+    torch.cuda.synchronize()
+    assert (U.from_dev(y2) == U.from_dev(y)).all()  # the halves are the fused call
+    ids_ref = oracle_mod.route(x, wr, b)[0]
+    _, offsets, perm_ref, inv_ref = oracle_mod.group(ids_ref, w.E)
+    assert (U.from_dev(perm) == perm_ref).all() and (U.from_dev(offs) == offsets).all()
+    yh, ygh = U.from_dev(y), U.from_dev(yg)
+    assert (yh == ygh[inv_ref]).all()
+    rows = U.sample_rows(offsets, 192)
+    x_g = oracle_mod.gather(x, perm_ref)
+    ref = oracle_mod.moe_ffn_permanent(x_g, offsets, *wl.make_experts(w),
+                                       *wl.make_permanent(w), rows=rows)
+    U.close(ygh[rows], ref, w.name)
+
+
+def test_zero_width_permanent_equals_plain_layer(L):
+    """P = 0 through the permanent entry points gives the plain layer's bits."""
+    w = wl.Workload("t", T=700, d=256, E=5, I=160, dtype="bf16")
+    x = U.to_dev(wl.make_x(w, 31))
+    ids = U.to_dev(np.random.default_rng(31).integers(0, w.E, size=w.T).astype(np.int32))
+    counts, offs, perm, inv, _ = L.readme_group_by_expert(ids, w.E)
+    wts = U.weights_to_dev(*wl.make_experts(w, 31))
+    empty = [torch.empty((0, w.d), dtype=torch.bfloat16, device=U.dev()) for _ in range(2)]
+    empty.append(torch.empty((w.d, 0), dtype=torch.bfloat16, device=U.dev()))
+    packed_p = L.readme_pack_experts_permanent(*wts, *empty)
+    packed = L.readme_pack_experts(*wts)
+    y0 = L.readme_moe_ffn_permanent_fused(x, perm, offs, packed_p, w.E, w.I, 0)
+    y1 = L.readme_moe_ffn_fused(x, perm, offs, packed, w.E, w.I)
+    torch.cuda.synchronize()
+    assert (U.from_dev(y0) == U.from_dev(y1)).all()
+
+
+def test_permanent_skips_unrouted_tokens(L, oracle_mod):
+    """Tokens with ids outside [0, E) get no output row (not even the
+    permanent term); routed rows match the oracle."""
+    T, d, E, I, P = 300, 128, 5, 96, 192
+    w = wl.Workload("t", T=T, d=d, E=E, I=I, P=P, dtype="bf16")
+    x = wl.make_x(w, 13)
+    ids_h = np.random.default_rng(13).integers(-1, E + 1, size=T).astype(np.int32)
+    counts, offs, perm, inv, _ = L.readme_group_by_expert(U.to_dev(ids_h), E)
+    y = torch.full((T, d), 7.0, dtype=torch.bfloat16, device=U.dev())
+    L.readme_moe_ffn_permanent_fused(U.to_dev(x), perm, offs, _pack(L, w, 13), E, I, P, y=y)
+    torch.cuda.synchronize()
+    yh = U.from_dev(y)
+    routed = (ids_h >= 0) & (ids_h < E)
+    assert (wl.bf16_bits_to_f32(yh[~routed]) == 7.0).all()
+    _, offsets, perm_ref, _ = oracle_mod.group(ids_h, E)
+    ref_g = oracle_mod.moe_ffn_permanent(oracle_mod.gather(x, perm_ref), offsets,
+                                         *wl.make_experts(w, 13), *wl.make_permanent(w, 13))
+    n = int(offsets[E])
+    U.close(yh[perm_ref[:n]], ref_g, "unrouted")
