@@ -165,7 +165,8 @@ int64_t readme_padded_intermediate(int64_t I);
  *     17 = 256x256, 18 = 128x256 (half-size K steps, deeper pipeline)
  *   weights streamed straight into registers (bf16; fp32 runs tile 6):
  *     12 = 128x256, 13 = 64x256, 14 = 32x256, 15 = 32x128 (deep pipeline),
- *     16 = 256x256, 19 = 128x256 (5 stages), 20 = 128x256 (6 stages)
+ *     16 = 256x256, 19 = 128x256 (5 stages), 20 = 128x256 (6 stages),
+ *     21 = 192x256 (3 stages), 22 = 192x256 (2 stages)
  *   (rows of tokens x columns of outputs)
  * Results do not depend on the tile beyond fp32 summation order.  Returns
  * README_ERR_ARG for any other value.  Not synchronised with calls in

@@ -18,17 +18,29 @@ bool set_gemm_tile(int tile) {
 // Tile shape by tokens per expert (the host knows T and E, not the split):
 // many rows per expert favour large tiles (fewer LDS and L2 bytes per
 // flop); few rows favour short tiles (no MFMA work on padding rows, more
-// workgroups to spread a weight stream over).  The down projection (N = d)
-// has more N tiles than gate/up at these shapes, so it switches to the
-// large tile earlier.  Thresholds come from tile sweeps on MI355X.
-static int tile_by_shape(bool gate_up, const GemmArgs& g) {
+// workgroups to spread a weight stream over).  The 192-row register-streamed
+// tile has the fewest load bytes per MFMA, so it pays where each tile has a
+// long K loop and its tile count still fills the CUs evenly; the LDS
+// 256x256 tile keeps the count lowest, which matters when a partial round
+// of tiles would remain.  Thresholds come from tile sweeps on MI355X over
+// the Llama-7B-shaped layer (with and without a permanent expert), the
+// 16-expert prefill and the d = 8192 request batch.
+static int tile_by_shape(bool f32, bool gate_up, const GemmArgs& g) {
     const int f = forced_tile();
     if (f > 0) return f;
     const int64_t per_expert = g.T / (g.E > 0 ? g.E : 1);
-    const int64_t big = gate_up ? 768 : 192;
-    if (per_expert >= big) return TILE_256x256;
-    if (per_expert >= 96) return gate_up ? TILE_BD_128x256 : TILE_128x256;
-    return TILE_BD_32x128;  // fp32 runs TILE_32x128 instead
+    if (f32) {  // both operands through LDS (the register-streamed kernel is bf16 only)
+        if (per_expert >= (gate_up ? 768 : 192)) return TILE_256x256;
+        return per_expert >= 96 && !gate_up ? TILE_128x256 : TILE_32x128;
+    }
+    if (per_expert < 96) return TILE_BD_32x128;
+    if (gate_up) {
+        if (g.shared_groups > 0) return TILE_256x256;  // every routed row once more per slice
+        if (per_expert >= 768) return g.K >= 8192 ? TILE_BD_192x256 : TILE_256x256;
+        return TILE_BD_128x256;
+    }
+    if (g.K >= 1024) return TILE_BD_192x256_S2;
+    return per_expert >= 192 ? TILE_256x256 : TILE_128x256;
 }
 
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s) {
@@ -38,7 +50,7 @@ hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s) {
     if (g.b_expert_stride * (f32 ? 4 : 2) > INT32_MAX) return hipErrorInvalidValue;
     if (g.K >= (int64_t)32 << 16) return hipErrorInvalidValue;
     if (g.k_segs > 1 && epi != EPI_STORE) return hipErrorInvalidValue;  // segments: down only
-    const int tile = tile_by_shape(epi == EPI_GATE_UP_SILU, g);
+    const int tile = tile_by_shape(f32, epi == EPI_GATE_UP_SILU, g);
     if (f32) {
         if (epi == EPI_GATE_UP_SILU) return launch_tile_f32_gate_up(tile, g, s);
         return launch_tile_f32_store(tile, g, s);

@@ -856,7 +856,9 @@ enum TileCfg {
     TILE_128x256_K32 = 18,  // 2x4 waves of 64x64, 6 half steps, 144 KB
     TILE_BD_128x256_S5 = 19,  // as 12, 5 K-steps in flight
     TILE_BD_128x256_S6 = 20,  // as 12, 6 K-steps in flight
-    TILE_LAST = TILE_BD_128x256_S6,
+    TILE_BD_192x256 = 21,     // 4 waves of 192x64, 3 K-steps
+    TILE_BD_192x256_S2 = 22,  // 4 waves of 192x64, 2 K-steps
+    TILE_LAST = TILE_BD_192x256_S2,
 };
 
 // Launches one tile configuration (instantiated per element type and
@@ -887,6 +889,8 @@ hipError_t launch_tile(int tile, GemmArgs g, hipStream_t s) {
             case TILE_BD_256x256: return launch_bd<256, 4, 2, 2, F32, EPI>(g, s);
             case TILE_BD_128x256_S5: return launch_bd<128, 4, 2, 5, F32, EPI>(g, s);
             case TILE_BD_128x256_S6: return launch_bd<128, 4, 2, 6, F32, EPI>(g, s);
+            case TILE_BD_192x256: return launch_bd<192, 4, 2, 3, F32, EPI>(g, s);
+            case TILE_BD_192x256_S2: return launch_bd<192, 4, 2, 2, F32, EPI>(g, s);
             default: break;
         }
     }
