@@ -190,6 +190,74 @@ def layer(x_res, offsets, w_gate, w_up, w_down, eps=1e-5, rows=None,
     return (y, xn) if want_xn else y
 
 
+def topk(logits: np.ndarray, K: int):
+    """Top-K experts per token and their gate weights (Eq. 2 with K > 1).
+
+    Selection decides integers, so it runs on the fp32 logits of ``route``
+    (the canonical order) and compares only: slot k takes, among the experts
+    not yet taken, the first one in ascending index order unless a later one
+    has a strictly larger logit -- top-1 is ``route``'s argmax, ties go to the
+    lower index and a NaN logit never beats another.  The weights are the
+    softmax of the selected logits (fp64), renormalised over the K slots, so
+    that K = 1 gives weight 1: the unweighted top-1 layer.
+    Returns ids [T][K] int32 (descending logit) and weights [T][K] float64.
+    """
+    logits = np.asarray(logits, np.float32)
+    T, E = logits.shape
+    if not 1 <= K <= E:
+        raise ValueError("need 1 <= K <= E")
+    taken = np.zeros((T, E), bool)
+    ids = np.empty((T, K), np.int32)
+    rows = np.arange(T)
+    for k in range(K):
+        best_id = np.full(T, -1, np.int64)
+        best = np.zeros(T, np.float32)
+        for e in range(E):
+            free = ~taken[:, e]
+            first = free & (best_id < 0)
+            better = free & (best_id >= 0) & (logits[:, e] > best)
+            pick = first | better
+            best_id = np.where(pick, e, best_id)
+            best = np.where(pick, logits[:, e], best)
+        ids[:, k] = best_id
+        taken[rows, best_id] = True
+    sel = logits[rows[:, None], ids].astype(np.float64)
+    z = np.exp(sel - sel[:, :1])
+    return ids, z / z.sum(axis=1, keepdims=True)
+
+
+def combine(y_g: np.ndarray, inv_perm: np.ndarray, weights: np.ndarray) -> np.ndarray:
+    """y[t] = sum over slots k (ascending) of weights[t,k] * y_g[inv_perm[t*K + k]],
+    fp64 (the gate-weighted sum of Eq. 2 over the K selected experts)."""
+    weights = np.asarray(weights, np.float64)
+    T, K = weights.shape
+    rows = np.asarray(inv_perm).reshape(T, K)
+    y = np.zeros((T, y_g.shape[1]), np.float64)
+    for k in range(K):
+        y += weights[:, k:k + 1] * np.asarray(y_g, np.float64)[rows[:, k]]
+    return y
+
+
+def full_path_topk(x, w_router, bias, w_gate, w_up, w_down, K: int, rows=None):
+    """route -> top-K -> group the T*K (token, slot) pairs -> expert FFN of each
+    pair -> gate-weighted combine.  Pair p = t*K + k carries token t's k-th
+    expert.  Returns ids [T][K], weights, counts, offsets, perm (pair index
+    per grouped row), inv_perm (grouped row per pair) and y (fp64; only the
+    listed token rows when ``rows`` is given, else all)."""
+    E = w_gate.shape[0]
+    _, logits = route(x, w_router, bias)
+    ids, wts = topk(logits, K)
+    counts, offsets, perm, inv = group(ids.reshape(-1), E)
+    T = x.shape[0]
+    toks = np.arange(T) if rows is None else np.asarray(rows, np.int64)
+    need = inv.reshape(T, K)[toks].reshape(-1)            # grouped rows those tokens use
+    x_pairs = np.ascontiguousarray(np.asarray(x)[perm // K])  # activation row of each pair
+    y_need = moe_ffn(x_pairs, offsets, w_gate, w_up, w_down, rows=need)
+    y = (wts[toks][:, :, None] * y_need.reshape(len(toks), K, -1)).sum(axis=1)
+    return dict(ids=ids, weights=wts, logits=logits, counts=counts, offsets=offsets,
+                perm=perm, inv_perm=inv, y=y)
+
+
 def threads() -> int:
     """OpenMP threads the oracle's parallel loops use."""
     return int(_load().oracle_threads())

@@ -48,7 +48,8 @@ class Workload:
     ``layers`` stacked layers sharing one routing (the pre-gating router runs
     once per step).  ``router`` is False when expert ids are given per request
     instead of computed.  ``P`` > 0 adds a permanent expert of P intermediate
-    neurons that every token passes through.
+    neurons that every token passes through; ``K`` > 1 routes each token to
+    its K highest-logit experts.
     """
     name: str
     T: int
@@ -57,6 +58,7 @@ class Workload:
     I: int
     dtype: str            # "f32" or "bf16"
     P: int = 0
+    K: int = 1
     layers: int = 1
     router: bool = True
     bias: str = "none"    # "none" | "zipf1" | "skew40_zipf1.2"
@@ -97,6 +99,12 @@ WORKLOADS = {
         description="Llama-7B-shaped MoE layer with a permanent expert: T=2048, "
                     "d=4096, E=8 routed experts of I=1376 plus P=1376 neurons "
                     "every token passes through, Zipf(1.0) router bias"),
+    "llama7b_layer_top2": Workload(
+        "llama7b_layer_top2", T=2048, d=4096, E=8, I=1376, K=2, dtype="bf16",
+        bias="zipf1",
+        description="Llama-7B-shaped MoE layer with top-2 routing: T=2048, "
+                    "d=4096, E=8, I=1376, each token on its two highest-logit "
+                    "experts with renormalised softmax weights"),
     "wide_requests": Workload(
         "wide_requests", T=8192, d=8192, E=8, I=3584, dtype="bf16",
         router=False, requests=256,
