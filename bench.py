@@ -81,19 +81,26 @@ class Path:
         self.bias = U.to_dev(b) if b is not None else None
         self.ids = (torch.empty(w.T, dtype=torch.int32, device=dev) if w.router
                     else U.to_dev(wl.make_request_ids(w, seed)))
+        # Top-K: router logits, then the T*K (token, slot) pairs are routed.
+        NP = w.T * w.K
+        if w.K > 1:
+            self.logits = torch.empty(w.T, w.E, dtype=torch.float32, device=dev)
+            self.pair_ids = torch.empty(NP, dtype=torch.int32, device=dev)
+            self.weights = torch.empty(NP, dtype=torch.float32, device=dev)
+            self.y_pairs = torch.empty(NP, w.d, dtype=self.x.dtype, device=dev)
         self.dt = _lib.README_F32 if w.dtype == "f32" else _lib.README_BF16
         i32 = torch.int32
         self.counts = torch.empty(w.E, dtype=i32, device=dev)
         self.offsets = torch.empty(w.E + 1, dtype=i32, device=dev)
-        self.perm = torch.empty(w.T, dtype=i32, device=dev)
-        self.inv = torch.empty(w.T, dtype=i32, device=dev)
+        self.perm = torch.empty(NP, dtype=i32, device=dev)
+        self.inv = torch.empty(NP, dtype=i32, device=dev)
         self.xg = torch.empty_like(self.x)
         self.yg = torch.empty_like(self.x)
         self.y = torch.empty_like(self.x)
         self.Ip = _lib.readme_padded_intermediate(w.I)
         # h holds the routed expert's neurons, then the permanent expert's
         # (P / I slices of one expert's width).
-        self.h = torch.empty(w.T, (1 + w.P // w.I) * self.Ip, dtype=self.x.dtype, device=dev)
+        self.h = torch.empty(NP, (1 + w.P // w.I) * self.Ip, dtype=self.x.dtype, device=dev)
         self.packed = []
         for layer in range(w.layers):
             wts = U.weights_to_dev(*wl.make_experts(w, seed, layer=layer))
@@ -129,7 +136,38 @@ class Path:
             return
         P, w = self.P, self.w
         self._ok(self.lib.readme_route(self.dt, w.T, w.d, w.E, P(self.x), P(self.wr),
-                                       P(self.bias), P(self.ids), None, self.stream), "route")
+                                       P(self.bias), P(self.ids),
+                                       P(self.logits) if w.K > 1 else None, self.stream),
+                 "route")
+
+    def topk(self):
+        P, w = self.P, self.w
+        self._ok(self.lib.readme_topk(w.T, w.E, w.K, P(self.logits), P(self.pair_ids),
+                                      P(self.weights), self.stream), "topk")
+
+    def group_pairs(self):
+        P, w = self.P, self.w
+        self._ok(self.lib.readme_group_by_expert(
+            w.T * w.K, w.E, P(self.pair_ids), P(self.counts), P(self.offsets), P(self.perm),
+            P(self.inv), self.dt, w.d, None, None, self.stream), "group")
+
+    def gate_up_pairs(self, k):
+        P, w = self.P, self.w
+        self._ok(self.lib.readme_moe_gate_up_gather_topk(
+            self.dt, w.T, w.d, w.E, w.I, w.K, P(self.x), P(self.perm), P(self.offsets),
+            P(self.packed[k]), P(self.h), self.stream), "gate_up_gather_topk")
+
+    def down_pairs(self, k):
+        P, w = self.P, self.w
+        self._ok(self.lib.readme_moe_down_scatter(
+            self.dt, w.T * w.K, w.d, w.E, w.I, P(self.h), P(self.perm), P(self.offsets),
+            P(self.packed[k]), P(self.y_pairs), self.stream), "down_scatter")
+
+    def combine(self):
+        P, w = self.P, self.w
+        self._ok(self.lib.readme_combine_topk(self.dt, w.T, w.d, w.K, P(self.y_pairs),
+                                              P(self.weights), P(self.y), self.stream),
+                 "combine")
 
     def group(self):
         P, w = self.P, self.w
@@ -207,6 +245,10 @@ class Path:
         if self.w.layers > 1:
             return [("route", self.route), ("group", self.group_resid),
                     ("stack", self.stack), ("ungroup", self.ungroup_resid)]
+        if self.w.K > 1:
+            return [("route", self.route), ("topk", self.topk), ("group", self.group_pairs),
+                    ("gate_up", lambda: self.gate_up_pairs(k)),
+                    ("down", lambda: self.down_pairs(k)), ("combine", self.combine)]
         if fused:
             return [("route", self.route), ("group", self.group_only),
                     ("gate_up", lambda: self.gate_up_gather(k)),
@@ -267,7 +309,13 @@ def algorithmic(w: wl.Workload, counts: np.ndarray, fused: bool = False) -> dict
             "ungroup": dict(bytes=2 * T * d * 4 + 4 * T, flops=0.0),
         }
     P = w.P  # permanent expert: P more neurons for every routed token
-    return {
+    # Top-K: n counts (token, slot) pairs; each pair's activation row is read
+    # and its output row written once, the combine reads K rows per token.
+    extra = {}
+    if w.K > 1:
+        extra = {"topk": dict(bytes=T * E * 4 + 8 * T * w.K, flops=0.0),
+                 "combine": dict(bytes=n * d * s + T * d * s + 4 * n, flops=2.0 * n * d)}
+    return {**extra,
         "route": dict(bytes=T * d * s + E * d * s + 4 * T, flops=2.0 * T * d * E),
         "group": dict(bytes=4 * T + 8 * T + 8 * E + (0 if fused else 2 * n * d * s), flops=0.0),
         "gate_up": dict(bytes=(active * I + P) * 2 * d * s + n * d * s + n * (I + P) * s,
@@ -293,7 +341,10 @@ def cpu_baseline(w: wl.Workload, target_s: float) -> dict:
     def run(S):
         ids = None if ids_all is None else ids_all[:S]
         t0 = time.perf_counter()
-        oracle.full_path(x_all[:S], wr, b, wg, wu, wd, ids=ids, permanent=perm_expert)
+        if w.K > 1:
+            oracle.full_path_topk(x_all[:S], wr, b, wg, wu, wd, K=w.K)
+        else:
+            oracle.full_path(x_all[:S], wr, b, wg, wu, wd, ids=ids, permanent=perm_expert)
         return time.perf_counter() - t0
 
     S = min(w.T, 16)
@@ -306,8 +357,9 @@ def cpu_baseline(w: wl.Workload, target_s: float) -> dict:
     return {"value": reps * S / total, "unit": "tokens/s", "cores": oracle.threads(),
             "kind": "oracle",
             "sample": f"first {S} of {w.T} tokens of the {w.name} workload, full path "
-                      f"(route, group, gather, fp64 expert FFN"
-                      f"{' + permanent expert' if w.P else ''}, ungroup), {reps} pass(es), "
+                      f"(route, {'top-%d, ' % w.K if w.K > 1 else ''}group, gather, fp64 expert FFN"
+                      f"{' + permanent expert' if w.P else ''}, "
+                      f"{'combine' if w.K > 1 else 'ungroup'}), {reps} pass(es), "
                       f"{total:.1f} s"}
 
 
@@ -323,8 +375,9 @@ def main():
         sys.exit(1)
 
     w = wl.WORKLOADS[args.workload]
-    if w.P and args.unfused:
-        print("bench.py: the permanent-expert workload runs the fused path only", file=sys.stderr)
+    if (w.P or w.K > 1) and args.unfused:
+        print("bench.py: the permanent-expert and top-K workloads run the fused path only",
+              file=sys.stderr)
         sys.exit(2)
     packed_bytes = 3 * (w.E + w.P // w.I) * (-(-w.I // 64) * 64) * w.d * w.elem_bytes
     copies = args.weight_copies or max(4, -(-(1 << 30) // packed_bytes))
@@ -393,7 +446,7 @@ def main():
     value = w.T * K / (gpu_ms / 1e3)  # tokens/s through one step
     if layers > 1:
         value = value * layers       # per MoE layer
-    ffn_flops = 6.0 * int(counts.sum()) * w.d * (w.I + w.P) * layers
+    ffn_flops = 6.0 * int(counts.sum()) * w.d * (w.I + w.P) * layers  # counts: rows (pairs)
 
     roof = None
     if dom_us:
@@ -413,6 +466,7 @@ def main():
         roof["kernel"] = ("readme_moe_ffn_stack (all layers)" if layers > 1
                           else "k_grouped_gemm (gate/up + SiLU*mul"
                           + (", permanent expert as extra row groups" if w.P else "")
+                          + (f", top-{w.K} (token, slot) pairs" if w.K > 1 else "")
                           + (", rows gathered through perm)" if fused else ")"))
         roof["launch_us"] = round(dom_us, 2)
         if dom == "gate_up" and fused and not args.gemm_tile:
@@ -433,7 +487,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32" if w.dtype == "f32" else "bf16",
         "data": "synthetic (seeded N(0,1) tokens, N(0,0.02) weights)",
-        "config": {"workload": w.name, "T": w.T, "d": w.d, "E": w.E, "I": w.I, "P": w.P,
+        "config": {"workload": w.name, "T": w.T, "d": w.d, "E": w.E, "I": w.I, "P": w.P, "K": w.K,
                    "gemm_tile": args.gemm_tile,
                    "row_moves": "separate" if args.unfused or layers > 1 else "fused into GEMMs",
                    "layers": layers, "weight_copies_rotated": ncopy,

@@ -335,6 +335,55 @@ readme_status readme_moe_ffn_permanent_fused(readme_dtype dt, int64_t T,
                                              void *stream);
 
 /*
+ * Top-K routing (Eq. 2 with K > 1): each token on its K highest-logit
+ * experts, the outputs summed with gate weights.  A step is
+ *   readme_route (with logits) -> readme_topk -> readme_group_by_expert over
+ *   the T*K (token, slot) pairs -> readme_moe_ffn_topk -> readme_combine_topk.
+ * Pair p = t*K + k carries token t's k-th expert; grouping the pairs gives
+ * perm (pair index per grouped row) and offsets over T*K rows.
+ *
+ * readme_topk -- ids[t*K + k] = the k-th expert of token t, weights[t*K + k]
+ *   its gate weight.  Slot k takes, among the experts not yet taken, the
+ *   first in ascending index unless a later one has a strictly larger logit
+ *   (top-1 = readme_route's argmax; ties to the lower index; a later NaN
+ *   never wins).  Weights: softmax of the K selected logits, renormalised
+ *   over the slots (fp32 expf), so K = 1 gives weight 1.
+ *   logits [T][E] fp32 (from readme_route), ids [T*K] int32, weights [T*K]
+ *   fp32 (device).  Requires 1 <= K <= E <= README_MAX_EXPERTS, T*K < 2^31.
+ * readme_moe_gate_up_gather_topk -- readme_moe_gate_up over the T*K grouped
+ *   pair rows, the activation row of grouped row j being x[perm[j] / K];
+ *   h [T*K][readme_padded_intermediate(I)] dt out.
+ * readme_moe_ffn_topk -- gate/up as above, then the down projection with
+ *   each grouped row's output written to its pair's row: y_pairs[perm[j]]
+ *   (y_pairs [T*K][d] dt, pair order: token t's K rows are adjacent).
+ *   workspace >= readme_moe_ffn_workspace_bytes(dt, T*K, I) bytes.
+ * readme_combine_topk -- y[t] = sum over k = 0 .. K-1 (in that order, fp32)
+ *   of weights[t*K + k] * y_pairs[t*K + k], rounded once to dt; K = 1
+ *   reproduces y_pairs bit for bit.  y [T][d] dt; d * element size a
+ *   multiple of 16 bytes.
+ * Errors as the single-expert entry points; K outside [1, E] is
+ * README_ERR_ARG.
+ */
+readme_status readme_topk(int64_t T, int32_t E, int32_t K, const float *logits,
+                          int32_t *ids, float *weights, void *stream);
+readme_status readme_moe_gate_up_gather_topk(readme_dtype dt, int64_t T,
+                                             int64_t d, int32_t E, int64_t I,
+                                             int32_t K, const void *x,
+                                             const int32_t *perm,
+                                             const int32_t *offsets,
+                                             const void *packed, void *h,
+                                             void *stream);
+readme_status readme_moe_ffn_topk(readme_dtype dt, int64_t T, int64_t d,
+                                  int32_t E, int64_t I, int32_t K, const void *x,
+                                  const int32_t *perm, const int32_t *offsets,
+                                  const void *packed, void *y_pairs,
+                                  void *workspace, size_t workspace_bytes,
+                                  void *stream);
+readme_status readme_combine_topk(readme_dtype dt, int64_t T, int64_t d, int32_t K,
+                                  const void *y_pairs, const float *weights,
+                                  void *y, void *stream);
+
+/*
  * readme_ungroup -- rows back to token order: y[t] = y_grouped[inv_perm[t]],
  * and a zero row where inv_perm[t] < 0 (an unrouted token).
  *   y_grouped [T][d] dt, inv_perm [T] int32, y [T][d] dt out.

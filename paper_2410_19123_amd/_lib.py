@@ -56,6 +56,12 @@ SIGNATURES = {
                                                    _P, _P, _P, _P]),
     "readme_moe_down_permanent_scatter": (_I32, [_I32, _I64, _I64, _I32, _I64, _I64, _P, _P, _P,
                                                  _P, _P, _P]),
+    "readme_topk": (_I32, [_I64, _I32, _I32, _P, _P, _P, _P]),
+    "readme_moe_gate_up_gather_topk": (_I32, [_I32, _I64, _I64, _I32, _I64, _I32, _P, _P, _P, _P,
+                                              _P, _P]),
+    "readme_moe_ffn_topk": (_I32, [_I32, _I64, _I64, _I32, _I64, _I32, _P, _P, _P, _P, _P, _P,
+                                   _SZ, _P]),
+    "readme_combine_topk": (_I32, [_I32, _I64, _I64, _I32, _P, _P, _P, _P]),
     "readme_ungroup": (_I32, [_I32, _I64, _I64, _P, _P, _P, _P]),
     "readme_moe_ffn_stack_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
     "readme_moe_ffn_stack": (_I32, [_I64, _I64, _I32, _I64, _I32, _P, _P, _P, _F, _P,
@@ -344,6 +350,59 @@ def readme_moe_down_permanent_scatter(h, perm, offsets, packed, E, I, P, d, y):
     _dev(h, perm, offsets, packed, y)
     _call("readme_moe_down_permanent_scatter", _dt(h), T, d, E, I, P, _p(h), _p(perm),
           _p(offsets), _p(packed), _p(y), _stream(h.device))
+    return y
+
+
+def readme_topk(logits, K, ids=None, weights=None):
+    """Top-K experts and renormalised gate weights from fp32 logits [T][E];
+    returns (ids [T*K] int32, weights [T*K] fp32)."""
+    T, E = logits.shape
+    if ids is None:
+        ids = torch.empty(T * K, dtype=torch.int32, device=logits.device)
+    if weights is None:
+        weights = torch.empty(T * K, dtype=torch.float32, device=logits.device)
+    _dev(logits, ids, weights)
+    if logits.dtype != torch.float32:
+        raise ValueError("logits must be fp32")
+    _call("readme_topk", T, E, K, _p(logits), _p(ids), _p(weights), _stream(logits.device))
+    return ids, weights
+
+
+def readme_moe_gate_up_gather_topk(x, perm, offsets, packed, E, I, K, h=None):
+    """Gate/up over the T*K grouped pair rows (activation row perm[j] // K)."""
+    T, d = x.shape
+    if h is None:
+        h = torch.empty(T * K, readme_padded_intermediate(I), dtype=x.dtype, device=x.device)
+    _dev(x, perm, offsets, packed, h)
+    _call("readme_moe_gate_up_gather_topk", _dt(x), T, d, E, I, K, _p(x), _p(perm), _p(offsets),
+          _p(packed), _p(h), _stream(x.device))
+    return h
+
+
+def readme_moe_ffn_topk(x, perm, offsets, packed, E, I, K, y_pairs=None, workspace=None):
+    """Expert FFN of every (token, slot) pair; returns y_pairs [T*K][d] in pair order."""
+    T, d = x.shape
+    if y_pairs is None:
+        y_pairs = torch.empty(T * K, d, dtype=x.dtype, device=x.device)
+    ws = readme_moe_ffn_workspace_bytes(x.dtype, T * K, I)
+    if workspace is None:
+        workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=x.device)
+    _dev(x, perm, offsets, packed, y_pairs, workspace)
+    _call("readme_moe_ffn_topk", _dt(x), T, d, E, I, K, _p(x), _p(perm), _p(offsets),
+          _p(packed), _p(y_pairs), _p(workspace), workspace.numel() * workspace.element_size(),
+          _stream(x.device))
+    return y_pairs
+
+
+def readme_combine_topk(y_pairs, weights, K, y=None):
+    """y[t] = sum_k weights[t*K+k] * y_pairs[t*K+k] (fp32, slot order)."""
+    TK, d = y_pairs.shape
+    T = TK // K
+    if y is None:
+        y = torch.empty(T, d, dtype=y_pairs.dtype, device=y_pairs.device)
+    _dev(y_pairs, weights, y)
+    _call("readme_combine_topk", _dt(y_pairs), T, d, K, _p(y_pairs), _p(weights), _p(y),
+          _stream(y_pairs.device))
     return y
 
 

@@ -362,6 +362,65 @@ readme_status readme_moe_down_permanent_scatter(readme_dtype dt, int64_t T, int6
                                      as_stream(stream)));
 }
 
+readme_status readme_topk(int64_t T, int32_t E, int32_t K, const float* logits, int32_t* ids,
+                          float* weights, void* stream) {
+    if (T < 0 || K < 1 || K > E) return README_ERR_ARG;
+    if (!experts_ok(E) || T * K > INT32_MAX) return README_ERR_UNSUPPORTED;
+    if (T == 0) return README_OK;
+    if (!logits || !ids || !weights) return README_ERR_ARG;
+    return hip_status(launch_topk(T, E, K, logits, ids, weights, as_stream(stream)));
+}
+
+readme_status readme_moe_gate_up_gather_topk(readme_dtype dt, int64_t T, int64_t d, int32_t E,
+                                             int64_t I, int32_t K, const void* x,
+                                             const int32_t* perm, const int32_t* offsets,
+                                             const void* packed, void* h, void* stream) {
+    if (K < 1 || K > E) return README_ERR_ARG;
+    if (T > INT32_MAX / K) return README_ERR_UNSUPPORTED;
+    readme_status st = check_ffn_shape(dt, T * K, d, E, I);
+    if (st != README_OK) return st;
+    if (T == 0) return README_OK;
+    if (!x || !perm || !offsets || !packed || !h) return README_ERR_ARG;
+    if (!a16(x) || !a16(packed) || !a16(h)) return README_ERR_ARG;
+    GemmArgs g = gate_up_args(dt, T * K, d, E, I, x, offsets, packed, h);
+    g.a_rows = perm;  // grouped row j is pair perm[j] = t*K + k, activation row t
+    g.a_rows_div = K;
+    return hip_status(
+        launch_grouped_gemm(dt == README_F32, EPI_GATE_UP_SILU, g, as_stream(stream)));
+}
+
+readme_status readme_moe_ffn_topk(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I,
+                                  int32_t K, const void* x, const int32_t* perm,
+                                  const int32_t* offsets, const void* packed, void* y_pairs,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+    if (K < 1 || K > E) return README_ERR_ARG;
+    if (T > INT32_MAX / K) return README_ERR_UNSUPPORTED;
+    readme_status st = check_ffn_shape(dt, T * K, d, E, I);
+    if (st != README_OK) return st;
+    if (T == 0) return README_OK;
+    if (!x || !perm || !offsets || !packed || !y_pairs || !workspace) return README_ERR_ARG;
+    if (!a16(y_pairs) || !a16(workspace)) return README_ERR_ARG;
+    if (workspace_bytes < readme_moe_ffn_workspace_bytes(dt, T * K, I)) return README_ERR_WORKSPACE;
+    st = readme_moe_gate_up_gather_topk(dt, T, d, E, I, K, x, perm, offsets, packed, workspace,
+                                        stream);
+    if (st != README_OK) return st;
+    // Each grouped row's output lands in its pair's row of y_pairs.
+    return readme_moe_down_scatter(dt, T * K, d, E, I, workspace, perm, offsets, packed, y_pairs,
+                                   stream);
+}
+
+readme_status readme_combine_topk(readme_dtype dt, int64_t T, int64_t d, int32_t K,
+                                  const void* y_pairs, const float* weights, void* y,
+                                  void* stream) {
+    if (!dtype_ok(dt) || T < 0 || d <= 0 || K < 1) return README_ERR_ARG;
+    if ((d * (int64_t)dtype_size(dt)) % 16 != 0 || K > README_MAX_EXPERTS) return README_ERR_UNSUPPORTED;
+    if (T == 0) return README_OK;
+    if (!y_pairs || !weights || !y) return README_ERR_ARG;
+    if (!a16(y_pairs) || !a16(y)) return README_ERR_ARG;
+    return hip_status(launch_combine(dt == README_F32, T, d, K, y_pairs, weights, y,
+                                     as_stream(stream)));
+}
+
 readme_status readme_ungroup(readme_dtype dt, int64_t T, int64_t d, const void* y_grouped,
                              const int32_t* inv_perm, void* y, void* stream) {
     if (!dtype_ok(dt) || T < 0 || d <= 0) return README_ERR_ARG;

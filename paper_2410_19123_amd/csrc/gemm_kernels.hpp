@@ -10,7 +10,9 @@
 //   EPI_STORE         B_e = W_down, output y;
 //   EPI_RESID_ADD     B_e = W_down, fp32 residual += y (stacked layers).
 // Optional row maps gather A rows (a_rows) and scatter output rows (c_rows),
-// which lets the row moves around the FFN ride inside the two GEMMs.
+// which lets the row moves around the FFN ride inside the two GEMMs; in a
+// top-K layer the gather map holds (token, slot) pairs and the A row is the
+// pair's token.
 //
 // Tiling.  A workgroup owns a BM x BN output tile of one expert; each of its
 // WGM x WGN waves owns a (BM/WGM) x (BN/WGN) sub-tile made of 32x32 MFMA
@@ -465,6 +467,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs args) {
         if (g.a_rows) {
             row = g.a_rows[row];
             row = (row >= 0 && row < g.T) ? row : 0;  // a corrupt map stays in bounds
+            if (g.a_rows_div > 1) row /= g.a_rows_div;  // pair -> token
         }
         a_src[i] = Ab + row * g.lda * ESZ + swzk(lane % KC, r) * 16;
     }
@@ -676,6 +679,7 @@ struct BdTile {
         if (g.a_rows) {
             row = g.a_rows[row];
             row = (row >= 0 && row < g.T) ? row : 0;  // a corrupt map stays in bounds
+            if (g.a_rows_div > 1) row /= g.a_rows_div;  // pair -> token
         }
         a_src[i] = Ab + row * g.lda * ESZ + swz(lane & 7, r) * 16;
         a_dst[i] = r * CPR + (lane & 7);
@@ -704,10 +708,6 @@ struct BdTile {
 #pragma unroll
         for (int i = 0; i < A_INS; ++i)
             aq[sl][i] = *reinterpret_cast<const u32x4*>(a_src[i] + (int64_t)kt * 128);
-    };
-    auto load = [&](auto sc, int kt) {
-        load_a(sc, kt);
-        load_b(sc, kt);
     };
     auto store_a = [&](auto sc, int buf) {
         constexpr int sl = decltype(sc)::value;

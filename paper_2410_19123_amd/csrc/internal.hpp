@@ -27,6 +27,9 @@ struct GemmArgs {
     // a_rows[j]; output row j is written to C row c_rows[j].  NULL = identity.
     const int32_t* a_rows;
     const int32_t* c_rows;
+    // a_rows_div > 1: a_rows holds (token, slot) pair indices t*div + k of a
+    // top-K layer, and the A row is the token, a_rows[j] / div.
+    int a_rows_div;
     // Permanent expert (neurons every routed token passes through), stored
     // as slices of one expert's shape at weight indices E, E+1, ...:
     //   shared_groups S > 0 (gate/up): S more row groups after the E experts,
@@ -59,6 +62,10 @@ hipError_t launch_pack_slots(readme_dtype dt, int64_t E_all, int64_t e0, int64_t
                              hipStream_t s);
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s);
 bool set_gemm_tile(int tile);
+hipError_t launch_topk(int64_t T, int E, int K, const float* logits, int32_t* ids, float* weights,
+                       hipStream_t s);
+hipError_t launch_combine(bool f32, int64_t T, int64_t d, int K, const void* y_pairs,
+                          const float* weights, void* y, hipStream_t s);
 hipError_t launch_rms_to_bf16(int64_t T, int64_t d, const float* x, const int32_t* offsets, int E,
                               float eps, uint16_t* xn, hipStream_t s);
 

@@ -127,3 +127,22 @@ def test_permanent_sizes_and_errors(lib):
     assert p(1, 8, 4096, 1376, 1376, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 100, None) == 3
     assert p(1, 8, 4096, 1376, 1376, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, big, None) == 1
     assert p(1, 8, 4096, 1376, 1000, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, big, None) == 2
+
+
+def test_topk_argument_errors(lib):
+    t = lib.readme_topk
+    assert t(16, 8, 0, FAKE, FAKE, FAKE, None) == 1        # K < 1
+    assert t(16, 8, 9, FAKE, FAKE, FAKE, None) == 1        # K > E
+    assert t(16, 300, 2, FAKE, FAKE, FAKE, None) == 2      # E > 256
+    assert t(16, 8, 2, None, FAKE, FAKE, None) == 1
+    assert t(0, 8, 2, None, None, None, None) == 0
+    f = lib.readme_moe_ffn_topk
+    big = 1 << 40
+    assert f(1, 16, 4096, 8, 1376, 2, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 10, None) == 3
+    assert f(1, 16, 4096, 8, 1376, 9, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, big, None) == 1
+    assert f(1, 1 << 30, 4096, 8, 1376, 4, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, big, None) == 2
+    assert lib.readme_moe_ffn_workspace_bytes(1, 2048 * 2, 1376) == 4096 * 1408 * 2
+    c = lib.readme_combine_topk
+    assert c(1, 16, 4, 2, FAKE, FAKE, FAKE, None) == 2     # 8-byte rows
+    assert c(1, 16, 64, 0, FAKE, FAKE, FAKE, None) == 1
+    assert c(1, 16, 64, 2, FAKE, None, FAKE, None) == 1
