@@ -23,7 +23,7 @@ bool set_gemm_tile(int tile) {
 // long K loop and its tile count still fills the CUs evenly; the LDS
 // 256x256 tile keeps the count lowest, which matters when a partial round
 // of tiles would remain.  Thresholds come from tile sweeps on MI355X over
-// the Llama-7B-shaped layer (with and without a permanent expert), the
+// the Llama-7B-shaped layer (top-1, top-2, with a permanent expert), the
 // 16-expert prefill and the d = 8192 request batch.
 static int tile_by_shape(bool f32, bool gate_up, const GemmArgs& g) {
     const int f = forced_tile();
@@ -35,9 +35,15 @@ static int tile_by_shape(bool f32, bool gate_up, const GemmArgs& g) {
     }
     if (per_expert < 96) return TILE_BD_32x128;
     if (gate_up) {
-        if (g.shared_groups > 0) return TILE_256x256;  // every routed row once more per slice
         if (per_expert >= 768) return g.K >= 8192 ? TILE_BD_192x256 : TILE_256x256;
-        return TILE_BD_128x256;
+        // 128-row tiles while their estimated count (half a tile of padding
+        // per row group) fits one round on the chip's 256 CUs; past that the
+        // 256-row tile's single round wins (permanent-expert groups, top-K
+        // pairs).
+        const int64_t groups = g.E + g.shared_groups;
+        const int64_t rows = g.T * (1 + g.shared_groups);
+        const int64_t est = (rows / 128 + groups / 2) * ceil_div(g.N, 256);
+        return est > 256 ? TILE_256x256 : TILE_BD_128x256;
     }
     if (g.K >= 1024) return TILE_BD_192x256_S2;
     return per_expert >= 192 ? TILE_256x256 : TILE_128x256;
