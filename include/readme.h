@@ -384,6 +384,54 @@ readme_status readme_combine_topk(readme_dtype dt, int64_t T, int64_t d, int32_t
                                   void *y, void *stream);
 
 /*
+ * Serving-side scheduling (Sec. 4), host code: no GPU, no streams; every
+ * pointer below is host memory, owned by the caller.
+ *
+ * readme_expert_batch -- expert-aware batching (Alg. 1): fills one batch of
+ *   at most max_tokens tokens from per-expert FIFO queues, repeatedly taking
+ *   the longest queue (lowest expert index on ties) whole while it fits in
+ *   the room left, else its first `room` tokens, then stopping; it also
+ *   stops when every queue is empty.  Queues: tokens of expert e are
+ *   queue_items[queue_offsets[e] .. queue_offsets[e+1]) (int32 ids, front
+ *   first).  Out: batch [max_tokens] (token ids in batch order),
+ *   *batch_len, taken [E] (tokens taken from the front of each queue; the
+ *   caller pops them), visited [E] (experts whose tokens entered the batch,
+ *   in order) and *n_visited.  Inputs are not modified.
+ *   README_ERR_ARG for E < 1, max_tokens < 0, decreasing offsets or a
+ *   missing array.
+ *
+ * readme_cache_simulate -- a demand cache of `capacity` entries over the
+ *   reference sequence refs [n] (int32 keys >= 0, e.g. layer * E + expert).
+ *   A reference hits if its key is cached; a miss inserts it, first
+ *   evicting, when the cache is full, by policy:
+ *     README_CACHE_BELADY  the cached key whose next reference is farthest
+ *                          ahead (never again = farthest), lowest key on
+ *                          ties: the rule of Sec. 4.1, exact because
+ *                          pre-gating makes the future references known;
+ *     README_CACHE_LRU     the least recently referenced key;
+ *     README_CACHE_FIFO    the earliest inserted key;
+ *     README_CACHE_RANDOM  the cached keys in ascending order, index
+ *                          r mod size, r the next SplitMix64 output from
+ *                          `seed` (Steele, Lea and Flood 2014).
+ *   Out: hits [n] (1 = hit), evicted [n] (the evicted key, -1 if none),
+ *   *n_hits.  O(n log capacity).  README_ERR_ARG for capacity < 1, n < 0, a
+ *   negative key, an unknown policy or a missing array.
+ */
+#define README_CACHE_BELADY 0
+#define README_CACHE_LRU 1
+#define README_CACHE_FIFO 2
+#define README_CACHE_RANDOM 3
+readme_status readme_expert_batch(int32_t E, const int32_t *queue_offsets,
+                                  const int32_t *queue_items, int64_t max_tokens,
+                                  int32_t *batch, int64_t *batch_len,
+                                  int32_t *taken, int32_t *visited,
+                                  int32_t *n_visited);
+readme_status readme_cache_simulate(int32_t policy, int64_t capacity, int64_t n,
+                                    const int32_t *refs, uint64_t seed,
+                                    uint8_t *hits, int32_t *evicted,
+                                    int64_t *n_hits);
+
+/*
  * readme_ungroup -- rows back to token order: y[t] = y_grouped[inv_perm[t]],
  * and a zero row where inv_perm[t] < 0 (an unrouted token).
  *   y_grouped [T][d] dt, inv_perm [T] int32, y [T][d] dt out.

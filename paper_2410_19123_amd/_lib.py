@@ -62,6 +62,8 @@ SIGNATURES = {
     "readme_moe_ffn_topk": (_I32, [_I32, _I64, _I64, _I32, _I64, _I32, _P, _P, _P, _P, _P, _P,
                                    _SZ, _P]),
     "readme_combine_topk": (_I32, [_I32, _I64, _I64, _I32, _P, _P, _P, _P]),
+    "readme_expert_batch": (_I32, [_I32, _P, _P, _I64, _P, _P, _P, _P, _P]),
+    "readme_cache_simulate": (_I32, [_I32, _I64, _I64, _P, ctypes.c_uint64, _P, _P, _P]),
     "readme_ungroup": (_I32, [_I32, _I64, _I64, _P, _P, _P, _P]),
     "readme_moe_ffn_stack_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
     "readme_moe_ffn_stack": (_I32, [_I64, _I64, _I32, _I64, _I32, _P, _P, _P, _F, _P,
@@ -404,6 +406,51 @@ def readme_combine_topk(y_pairs, weights, K, y=None):
     _call("readme_combine_topk", _dt(y_pairs), T, d, K, _p(y_pairs), _p(weights), _p(y),
           _stream(y_pairs.device))
     return y
+
+
+README_CACHE_POLICIES = {"belady": 0, "lru": 1, "fifo": 2, "random": 3}
+
+
+def _host_i32(a):
+    import numpy as np
+    a = np.ascontiguousarray(a, dtype=np.int32)
+    return a, a.ctypes.data_as(ctypes.c_void_p)
+
+
+def readme_expert_batch(queues, max_tokens: int):
+    """Alg. 1 on host lists of per-expert token queues; returns
+    (batch list, taken per expert, visited experts)."""
+    import numpy as np
+    E = len(queues)
+    offs = np.zeros(E + 1, np.int64)
+    offs[1:] = np.cumsum([len(q) for q in queues])
+    offs, p_offs = _host_i32(offs)
+    items, p_items = _host_i32(np.concatenate([np.asarray(q, np.int64) for q in queues])
+                               if offs[-1] else np.zeros(1))
+    batch = np.zeros(max(max_tokens, 1), np.int32)
+    taken = np.zeros(E, np.int32)
+    visited = np.zeros(E, np.int32)
+    blen, nv = ctypes.c_int64(0), ctypes.c_int32(0)
+    _call("readme_expert_batch", E, p_offs, p_items, max_tokens,
+          batch.ctypes.data_as(ctypes.c_void_p), ctypes.byref(blen),
+          taken.ctypes.data_as(ctypes.c_void_p), visited.ctypes.data_as(ctypes.c_void_p),
+          ctypes.byref(nv))
+    return batch[:blen.value].tolist(), taken.tolist(), visited[:nv.value].tolist()
+
+
+def readme_cache_simulate(refs, capacity: int, policy: str, seed: int = 0):
+    """Cache replacement over a host reference sequence; returns
+    (hits [n] bool, evicted [n] int, number of hits)."""
+    import numpy as np
+    refs, p_refs = _host_i32(refs)
+    n = refs.shape[0]
+    hits = np.zeros(max(n, 1), np.uint8)
+    evicted = np.zeros(max(n, 1), np.int32)
+    nh = ctypes.c_int64(0)
+    _call("readme_cache_simulate", README_CACHE_POLICIES[policy], capacity, n, p_refs, seed,
+          hits.ctypes.data_as(ctypes.c_void_p), evicted.ctypes.data_as(ctypes.c_void_p),
+          ctypes.byref(nh))
+    return hits[:n].astype(bool).tolist(), evicted[:n].tolist(), nh.value
 
 
 def readme_ungroup(y_grouped, inv_perm, y=None):

@@ -201,6 +201,24 @@ def make_request_ids(w: Workload, seed: int = 0) -> np.ndarray:
     return np.repeat(req, per).astype(np.int32)
 
 
+def make_locality_ids(steps: int, batch: int, E: int, seed: int = 0,
+                      keep: float = 2921 / 4096, zipf: float = 1.0) -> np.ndarray:
+    """Expert ids [steps][batch] of decode requests with temporal locality:
+    each request keeps its previous token's expert with probability `keep`
+    (2921/4096, the share of tokens that follow the previous token's expert
+    reported in Sec. 5.3), else draws one with probability proportional to
+    (e+1)^-zipf."""
+    rng = np.random.default_rng([seed, 0x5EED])
+    p = 1.0 / np.arange(1, E + 1, dtype=np.float64) ** zipf
+    p /= p.sum()
+    ids = np.empty((steps, batch), np.int32)
+    ids[0] = rng.choice(E, size=batch, p=p)
+    for s in range(1, steps):
+        stay = rng.random(batch) < keep
+        ids[s] = np.where(stay, ids[s - 1], rng.choice(E, size=batch, p=p))
+    return ids
+
+
 def make_dense(w: Workload, seed: int = 0, layer: int = 0):
     """The dense FFN the experts are sliced from: (W_gate[D][d], W_up[D][d],
     W_down[d][D]) with D = E*I + P, in the workload's dtype."""
@@ -249,5 +267,5 @@ def describe(w: Workload) -> str:
 __all__ = [
     "Workload", "WORKLOADS", "normal", "to_bf16_bits", "bf16_bits_to_f32",
     "router_bias", "make_x", "make_router", "make_request_ids",
-    "make_experts", "make_permanent", "make_dense", "flops_per_layer", "describe", "SKEW_BIAS0",
+    "make_experts", "make_permanent", "make_dense", "make_locality_ids", "flops_per_layer", "describe", "SKEW_BIAS0",
 ]

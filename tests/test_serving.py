@@ -1,0 +1,155 @@
+"""Serving-side scheduling (Sec. 4): the oracle pinned by hand-derived
+batches (Alg. 1), textbook page-replacement counts and exhaustive optimal
+eviction on tiny traces; the library's host implementation equal to the
+oracle on random inputs (no GPU needed)."""
+import functools
+import os
+
+import numpy as np
+import pytest
+
+from oracle import serving as S
+from paper_2410_19123_amd import workloads as wl
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+REF = [1, 2, 3, 4, 1, 2, 5, 1, 2, 3, 4, 5]
+
+
+def _ints(txt):
+    txt = txt.strip()
+    return [int(v) for v in txt.split(",")] if txt else []
+
+
+def _golden_alg1():
+    for line in open(os.path.join(GOLD, "alg1_batches.txt")):
+        if not line.strip() or line.startswith("#"):
+            continue
+        q, m, batch, taken, visited = [f.strip() for f in line.split(";")]
+        yield [_ints(x) for x in q.split("|")], int(m), _ints(batch), _ints(taken), _ints(visited)
+
+
+def test_alg1_hand_derived():
+    for queues, m, batch, taken, visited in _golden_alg1():
+        assert S.expert_batch(queues, m) == (batch, taken, visited), (queues, m)
+
+
+def test_cache_textbook_counts():
+    for line in open(os.path.join(GOLD, "cache_textbook.txt")):
+        if not line.strip() or line.startswith("#"):
+            continue
+        policy, cap, misses = [f.strip() for f in line.split(";")]
+        hits, _ = S.cache_simulate(REF, int(cap), policy)
+        assert hits.count(False) == int(misses), (policy, cap)
+
+
+def _optimal_misses(refs, cap):
+    """Fewest misses over every eviction choice (exhaustive, tiny inputs)."""
+    @functools.lru_cache(maxsize=None)
+    def go(t, cache):
+        if t == len(refs):
+            return 0
+        if refs[t] in cache:
+            return go(t + 1, cache)
+        if len(cache) < cap:
+            return 1 + go(t + 1, tuple(sorted(cache + (refs[t],))))
+        return 1 + min(go(t + 1, tuple(sorted(tuple(c for c in cache if c != v) + (refs[t],))))
+                       for v in cache)
+    return go(0, ())
+
+
+def test_belady_is_optimal_on_tiny_traces():
+    rng = np.random.default_rng(3)
+    for _ in range(60):
+        n = int(rng.integers(1, 13))
+        keys = int(rng.integers(2, 6))
+        cap = int(rng.integers(1, 4))
+        refs = rng.integers(0, keys, size=n).tolist()
+        hits, _ = S.cache_simulate(refs, cap, "belady")
+        assert hits.count(False) == _optimal_misses(refs, cap), (refs, cap)
+
+
+def _locality_trace(steps, E, L, seed):
+    """Expert-layer references of a decode batch whose tokens keep their
+    expert with probability 2921/4096 (the temporal locality reported in
+    Sec. 5.3), else draw a Zipf-weighted one."""
+    ids = wl.make_locality_ids(steps, 8, E, seed)
+    refs = []
+    for s in range(steps):
+        for layer in range(L):
+            refs.extend(layer * E + e for e in sorted(set(ids[s].tolist())))
+    return refs
+
+
+def test_belady_beats_baselines():
+    rng = np.random.default_rng(5)
+    traces = [rng.integers(0, 12, size=300).tolist(), _locality_trace(40, 8, 4, 1)]
+    for refs in traces:
+        for cap in (2, 5, 9):
+            best = S.cache_simulate(refs, cap, "belady")[0].count(True)
+            for p in ("lru", "fifo", "random"):
+                assert best >= S.cache_simulate(refs, cap, p, seed=7)[0].count(True), (p, cap)
+
+
+def test_splitmix64_reference_values():
+    # First outputs from state 0 (the generator's published test vector).
+    st, a = S.splitmix64(0)
+    st, b = S.splitmix64(st)
+    assert a == 0xE220A8397B1DCDAF and b == 0x6E789E6AA1B965F4
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2410_19123_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.skip("libreadme.so not built")
+    _lib.load()
+    return _lib
+
+
+def test_native_alg1_equals_oracle(lib):
+    for queues, m, batch, taken, visited in _golden_alg1():
+        assert lib.readme_expert_batch(queues, m) == (batch, taken, visited)
+    rng = np.random.default_rng(11)
+    tok = 0
+    for _ in range(300):
+        E = int(rng.integers(1, 10))
+        queues = []
+        for _e in range(E):
+            k = int(rng.integers(0, 12))
+            queues.append(list(range(tok, tok + k)))
+            tok += k
+        m = int(rng.integers(0, 40))
+        assert lib.readme_expert_batch(queues, m) == S.expert_batch(queues, m), (queues, m)
+
+
+def test_native_cache_equals_oracle(lib):
+    rng = np.random.default_rng(13)
+    traces = [REF, _locality_trace(30, 8, 3, 2)]
+    traces += [rng.integers(0, int(rng.integers(1, 20)), size=int(rng.integers(0, 200))).tolist()
+               for _ in range(40)]
+    for refs in traces:
+        for cap in (1, 2, 3, 7):
+            for p in ("belady", "lru", "fifo", "random"):
+                h, ev = S.cache_simulate(refs, cap, p, seed=99)
+                gh, gev, nh = lib.readme_cache_simulate(refs, cap, p, seed=99)
+                assert (gh, gev, nh) == (h, ev, h.count(True)), (p, cap, refs[:20])
+
+
+def test_native_argument_errors(lib):
+    import ctypes
+    L = lib.load()
+    n = ctypes.c_int64(0)
+    assert L.readme_cache_simulate(0, 0, 0, None, 0, None, None, ctypes.byref(n)) == 1
+    assert L.readme_cache_simulate(9, 2, 0, None, 0, None, None, ctypes.byref(n)) == 1
+    bad = (ctypes.c_int32 * 1)(-3)
+    h = (ctypes.c_uint8 * 1)()
+    ev = (ctypes.c_int32 * 1)()
+    assert L.readme_cache_simulate(0, 2, 1, bad, 0, h, ev, ctypes.byref(n)) == 1
+    offs = (ctypes.c_int32 * 3)(0, 2, 1)   # decreasing
+    items = (ctypes.c_int32 * 2)(5, 6)
+    out = (ctypes.c_int32 * 4)()
+    bl, nv = ctypes.c_int64(0), ctypes.c_int32(0)
+    assert L.readme_expert_batch(2, offs, items, 4, out, ctypes.byref(bl), out, out,
+                                 ctypes.byref(nv)) == 1
+    assert L.readme_expert_batch(0, offs, items, 4, out, ctypes.byref(bl), out, out,
+                                 ctypes.byref(nv)) == 1
