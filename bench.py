@@ -62,6 +62,41 @@ def parse():
     return ap.parse_args()
 
 
+def serving_schedule(w: wl.Workload, steps: int, lib, seed: int = 0):
+    """Expert ids [steps][T] of the decode batches a serving loop forms from
+    w.pool waiting requests: first-come first-served, or expert-aware
+    batching (Alg. 1, the library's readme_expert_batch).  After a step each
+    scheduled request's next token re-enters the pool at the back, keeping
+    its expert with probability 2921/4096 (the locality reported in
+    Sec. 5.3), else drawing one with probability proportional to 1/(e+1)."""
+    import collections
+    expert, rng, p = wl.make_pool(w, seed)
+    expert = expert.tolist()
+    queues = [collections.deque() for _ in range(w.E)]
+    arrival = collections.deque(range(w.pool))
+    for r in range(w.pool):
+        queues[expert[r]].append(r)
+    out = np.empty((steps, w.T), np.int32)
+    for st in range(steps):
+        if w.batching == "alg1":
+            batch, taken, _ = lib.readme_expert_batch([list(q) for q in queues], w.T)
+            for e in range(w.E):
+                for _ in range(taken[e]):
+                    queues[e].popleft()
+        else:
+            batch = [arrival.popleft() for _ in range(w.T)]
+        out[st] = [expert[r] for r in batch]
+        keep = rng.random(len(batch)) < 2921 / 4096
+        fresh = rng.choice(w.E, size=len(batch), p=p)
+        for j, r in enumerate(batch):
+            expert[r] = expert[r] if keep[j] else int(fresh[j])
+            if w.batching == "alg1":
+                queues[expert[r]].append(r)
+            else:
+                arrival.append(r)
+    return out
+
+
 class Path:
     """Pre-marshalled C-ABI calls of one step (host overhead kept small so
     that the GPU, not Python, sets the pace)."""
@@ -79,8 +114,14 @@ class Path:
         wr, b = wl.make_router(w, seed)
         self.wr = U.to_dev(wr) if wr is not None else None
         self.bias = U.to_dev(b) if b is not None else None
-        self.ids = (torch.empty(w.T, dtype=torch.int32, device=dev) if w.router
-                    else U.to_dev(wl.make_request_ids(w, seed)))
+        if w.batching:
+            # one scheduled batch per weight copy (the copies are the layers)
+            self.sched = serving_schedule(w, max(w.layers, 1), _lib, seed)
+            self.sched_ids = U.to_dev(self.sched)
+            self.ids = self.sched_ids[0]
+        else:
+            self.ids = (torch.empty(w.T, dtype=torch.int32, device=dev) if w.router
+                        else U.to_dev(wl.make_request_ids(w, seed)))
         # Top-K: router logits, then the T*K (token, slot) pairs are routed.
         NP = w.T * w.K
         if w.K > 1:
@@ -192,11 +233,13 @@ class Path:
         self._ok(self.lib.readme_ungroup(self.dt, w.T, w.d, P(self.yg), P(self.inv), P(self.y),
                                          self.stream), "ungroup")
 
-    def group_resid(self):
-        """Group tokens and gather the fp32 residual rows into grouped order."""
+    def group_resid(self, k=0):
+        """Group tokens and gather the fp32 residual rows into grouped order
+        (a serving loop's k-th scheduled batch when batches are scheduled)."""
         P, w = self.P, self.w
+        ids = self.sched_ids[k % self.sched_ids.shape[0]] if w.batching else self.ids
         self._ok(self.lib.readme_group_by_expert(
-            w.T, w.E, P(self.ids), P(self.counts), P(self.offsets), P(self.perm), P(self.inv),
+            w.T, w.E, P(ids), P(self.counts), P(self.offsets), P(self.perm), P(self.inv),
             0, w.d, P(self.x32), P(self.xres), self.stream), "group")
 
     def stack(self):
@@ -243,7 +286,7 @@ class Path:
         """(name, call) of one step, in path order; k picks the weight copy.
         fused: the row gather and the ungroup ride in the two GEMMs."""
         if self.w.layers > 1:
-            return [("route", self.route), ("group", self.group_resid),
+            return [("route", self.route), ("group", lambda: self.group_resid(k)),
                     ("stack", self.stack), ("ungroup", self.ungroup_resid)]
         if self.w.K > 1:
             return [("route", self.route), ("topk", self.topk), ("group", self.group_pairs),
@@ -336,7 +379,12 @@ def cpu_baseline(w: wl.Workload, target_s: float) -> dict:
     wr, b = wl.make_router(w)
     wg, wu, wd = wl.make_experts(w)
     perm_expert = wl.make_permanent(w) if w.P else None
-    ids_all = None if w.router else wl.make_request_ids(w)
+    if w.router:
+        ids_all = None
+    elif w.batching:
+        ids_all = wl.make_pool(w)[0]   # the waiting requests' experts
+    else:
+        ids_all = wl.make_request_ids(w)
 
     def run(S):
         ids = None if ids_all is None else ids_all[:S]
@@ -440,13 +488,20 @@ def main():
 
     counts = path.counts.cpu().numpy()
     work = algorithmic(w, counts, fused)
+    if w.batching:
+        # the batches differ from step to step: average their work
+        per = [algorithmic(w, np.bincount(b, minlength=w.E), fused) for b in path.sched]
+        work = {n: {q: float(np.mean([pw[n][q] for pw in per])) for q in ("bytes", "flops")}
+                for n in per[0]}
+        counts = np.bincount(path.sched.reshape(-1), minlength=w.E) // path.sched.shape[0]
     kern_us = {n: (1e3 * float(np.mean([a.elapsed_time(b) for a, b in ev[n]])) if ev[n] else None)
                for n in names}
 
     value = w.T * K / (gpu_ms / 1e3)  # tokens/s through one step
     if layers > 1:
         value = value * layers       # per MoE layer
-    ffn_flops = 6.0 * int(counts.sum()) * w.d * (w.I + w.P) * layers  # counts: rows (pairs)
+    rows = w.T if w.batching else int(counts.sum())  # routed rows (pairs for top-K)
+    ffn_flops = 6.0 * rows * w.d * (w.I + w.P) * layers
 
     roof = None
     if dom_us:
@@ -491,7 +546,11 @@ def main():
                    "gemm_tile": args.gemm_tile,
                    "row_moves": "separate" if args.unfused or layers > 1 else "fused into GEMMs",
                    "layers": layers, "weight_copies_rotated": ncopy,
-                   "tokens_per_expert": counts.tolist()},
+                   "tokens_per_expert": counts.tolist(),
+                   **({"batching": w.batching, "pool": w.pool,
+                       "unique_experts_per_batch": round(float(np.mean(
+                           [len(set(b.tolist())) for b in path.sched])), 2)}
+                      if w.batching else {})},
         "ffn_tflops": round(ffn_flops / (ms_per_step * 1e-3) / 1e12, 2),
         # event pair before each call, from a separate 20-step pass after the
         # timed region (events between every call add their own gaps)

@@ -59,6 +59,8 @@ class Workload:
     dtype: str            # "f32" or "bf16"
     P: int = 0
     K: int = 1
+    batching: str = ""    # "alg1" | "fifo": batches drawn from a pool of waiting requests
+    pool: int = 0         # waiting decode requests the batches are drawn from
     layers: int = 1
     router: bool = True
     bias: str = "none"    # "none" | "zipf1" | "skew40_zipf1.2"
@@ -88,6 +90,18 @@ WORKLOADS = {
         layers=32, bias="zipf1",
         description="decode step: 64 tokens through 32 stacked Llama-7B-"
                     "shaped MoE layers, routed once"),
+    "llama7b_decode32_alg1": Workload(
+        "llama7b_decode32_alg1", T=64, d=4096, E=8, I=1376, dtype="bf16",
+        layers=32, router=False, batching="alg1", pool=1024,
+        description="serving loop: 64-token decode batches formed by expert-aware "
+                    "batching (Alg. 1) from 1024 waiting requests, 32 stacked "
+                    "Llama-7B-shaped MoE layers"),
+    "llama7b_decode32_fifo": Workload(
+        "llama7b_decode32_fifo", T=64, d=4096, E=8, I=1376, dtype="bf16",
+        layers=32, router=False, batching="fifo", pool=1024,
+        description="serving loop: 64-token decode batches taken first-come "
+                    "first-served from 1024 waiting requests, 32 stacked "
+                    "Llama-7B-shaped MoE layers"),
     "prefill_skew16": Workload(
         "prefill_skew16", T=16384, d=4096, E=16, I=688, dtype="bf16",
         bias="skew40_zipf1.2",
@@ -219,6 +233,16 @@ def make_locality_ids(steps: int, batch: int, E: int, seed: int = 0,
     return ids
 
 
+def make_pool(w: Workload, seed: int = 0):
+    """Expert id of each of the w.pool waiting requests (probability
+    proportional to 1/(e+1)) and the random stream that draws their later
+    tokens' experts."""
+    rng = np.random.default_rng([seed, 0xB47C])
+    p = 1.0 / np.arange(1, w.E + 1, dtype=np.float64)
+    p /= p.sum()
+    return rng.choice(w.E, size=w.pool, p=p).astype(np.int32), rng, p
+
+
 def make_dense(w: Workload, seed: int = 0, layer: int = 0):
     """The dense FFN the experts are sliced from: (W_gate[D][d], W_up[D][d],
     W_down[d][D]) with D = E*I + P, in the workload's dtype."""
@@ -267,5 +291,5 @@ def describe(w: Workload) -> str:
 __all__ = [
     "Workload", "WORKLOADS", "normal", "to_bf16_bits", "bf16_bits_to_f32",
     "router_bias", "make_x", "make_router", "make_request_ids",
-    "make_experts", "make_permanent", "make_dense", "make_locality_ids", "flops_per_layer", "describe", "SKEW_BIAS0",
+    "make_experts", "make_permanent", "make_dense", "make_locality_ids", "make_pool", "flops_per_layer", "describe", "SKEW_BIAS0",
 ]
