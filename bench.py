@@ -155,6 +155,10 @@ class Path:
         if w.layers == 1:
             for _ in range(copies - 1):
                 self.packed.append(self.packed[0].clone())
+        self.ex = None
+        if w.offload_slots:
+            # Weights live in pinned host memory behind a device slot cache.
+            self.ex = _lib.Offload(self.packed, w.E, w.d, w.I, w.offload_slots, w.policy)
         if w.layers > 1:
             # The stack's residual stream is fp32; the router reads bf16 features.
             self.x32 = self.x.float()
@@ -249,6 +253,14 @@ class Path:
             P(self.offsets), P(self.xres), ctypes.c_float(1e-5), P(self.ws),
             self.ws.numel(), self.stream), "stack")
 
+    def offload_stack(self, k):
+        """The stack through the offload executor; the host knows each
+        scheduled batch's expert counts (and the next one's)."""
+        n = self.sched.shape[0]
+        cnt = np.bincount(self.sched[k % n], minlength=self.w.E)
+        nxt = np.bincount(self.sched[(k + 1) % n], minlength=self.w.E)
+        self.ex.stack(self.xres, self.offsets, cnt, nxt, workspace=self.ws)
+
     def ungroup_resid(self):
         P, w = self.P, self.w
         self._ok(self.lib.readme_ungroup(0, w.T, w.d, P(self.xres), P(self.inv),
@@ -286,8 +298,9 @@ class Path:
         """(name, call) of one step, in path order; k picks the weight copy.
         fused: the row gather and the ungroup ride in the two GEMMs."""
         if self.w.layers > 1:
+            stack = (lambda: self.offload_stack(k)) if self.ex else self.stack
             return [("route", self.route), ("group", lambda: self.group_resid(k)),
-                    ("stack", self.stack), ("ungroup", self.ungroup_resid)]
+                    ("stack", stack), ("ungroup", self.ungroup_resid)]
         if self.w.K > 1:
             return [("route", self.route), ("topk", self.topk), ("group", self.group_pairs),
                     ("gate_up", lambda: self.gate_up_pairs(k)),
@@ -488,6 +501,14 @@ def main():
 
     counts = path.counts.cpu().numpy()
     work = algorithmic(w, counts, fused)
+    offload = None
+    if path.ex:
+        hits, misses, nbytes = path.ex.stats()
+        steps_run = W + K + min(K, 20)
+        offload = {"slots": w.offload_slots, "policy": w.policy,
+                   "hit_ratio": round(hits / max(hits + misses, 1), 4),
+                   "gb_copied_per_step": round(nbytes / steps_run / 1e9, 3),
+                   "h2d_gb_s": round(nbytes / steps_run / (ms_per_step * 1e-3) / 1e9, 1)}
     if w.batching:
         # the batches differ from step to step: average their work
         per = [algorithmic(w, np.bincount(b, minlength=w.E), fused) for b in path.sched]
@@ -550,7 +571,8 @@ def main():
                    **({"batching": w.batching, "pool": w.pool,
                        "unique_experts_per_batch": round(float(np.mean(
                            [len(set(b.tolist())) for b in path.sched])), 2)}
-                      if w.batching else {})},
+                      if w.batching else {}),
+                   **({"offload": offload} if offload else {})},
         "ffn_tflops": round(ffn_flops / (ms_per_step * 1e-3) / 1e12, 2),
         # event pair before each call, from a separate 20-step pass after the
         # timed region (events between every call add their own gaps)

@@ -432,6 +432,50 @@ readme_status readme_cache_simulate(int32_t policy, int64_t capacity, int64_t n,
                                     int64_t *n_hits);
 
 /*
+ * Expert offload for the layer stack (Sec. 4.1: pre-gating lets the exact
+ * experts of every layer be fetched ahead, and the cache replace by the
+ * Belady rule).  The packed experts of every layer live in pinned host
+ * memory; a device cache of `slots` (layer, expert) slots holds the weights
+ * the GEMMs read; a second stream of the library's own (default priority)
+ * copies the experts of layer l+1 while the caller's stream computes layer l.
+ *
+ * readme_offload_create -- copies the L packed layers (device buffers from
+ *   readme_pack_experts, bf16, E experts of width I at d; the caller may
+ *   free them afterwards) into pinned host memory and allocates the slots
+ *   (slots * 3 * readme_padded_intermediate(I) * d * 2 bytes).  policy:
+ *   README_CACHE_BELADY or README_CACHE_LRU.  Set-up call: it allocates and
+ *   waits for its copies on `stream`.
+ * readme_offload_stack -- readme_moe_ffn_stack over the L layers with the
+ *   weights fetched through the cache: same kernels, same results bit for
+ *   bit.  counts [E] (host) are the token counts of `offsets` (the caller's
+ *   scheduler knows them: no device read), next_counts [E] (host, or NULL)
+ *   those of the next step, which the Belady rule looks ahead to.  Needs
+ *   slots >= 2 * (experts with tokens); else README_ERR_UNSUPPORTED.  A
+ *   miss evicts, among slots not used by the layer being loaded or the layer
+ *   before it, the key referenced farthest ahead (lowest key on ties) or the
+ *   least recently referenced one.  Host side: plans the whole step, then
+ *   enqueues; it waits on the host only for the copy of its slot table from
+ *   two steps earlier.  Calls on one executor must not overlap.
+ * readme_offload_stats -- cumulative hits, misses and bytes copied.
+ * readme_offload_destroy -- waits for the executor's copies and for the last
+ *   recorded layer of the compute stream, then frees everything.
+ */
+typedef struct readme_offload readme_offload;
+readme_status readme_offload_create(int32_t E, int64_t d, int64_t I, int32_t L,
+                                    int32_t slots, int32_t policy,
+                                    const void *const *packed_layers,
+                                    readme_offload **out, void *stream);
+readme_status readme_offload_stack(readme_offload *ex, int64_t T,
+                                   const int32_t *offsets, const int32_t *counts,
+                                   const int32_t *next_counts,
+                                   float *x_resid_grouped, float rms_eps,
+                                   void *workspace, size_t workspace_bytes,
+                                   void *stream);
+readme_status readme_offload_stats(const readme_offload *ex, int64_t *hits,
+                                   int64_t *misses, int64_t *bytes_copied);
+void readme_offload_destroy(readme_offload *ex);
+
+/*
  * readme_ungroup -- rows back to token order: y[t] = y_grouped[inv_perm[t]],
  * and a zero row where inv_perm[t] < 0 (an unrouted token).
  *   y_grouped [T][d] dt, inv_perm [T] int32, y [T][d] dt out.

@@ -64,6 +64,10 @@ SIGNATURES = {
     "readme_combine_topk": (_I32, [_I32, _I64, _I64, _I32, _P, _P, _P, _P]),
     "readme_expert_batch": (_I32, [_I32, _P, _P, _I64, _P, _P, _P, _P, _P]),
     "readme_cache_simulate": (_I32, [_I32, _I64, _I64, _P, ctypes.c_uint64, _P, _P, _P]),
+    "readme_offload_create": (_I32, [_I32, _I64, _I64, _I32, _I32, _I32, _P, _P, _P]),
+    "readme_offload_stack": (_I32, [_P, _I64, _P, _P, _P, _P, _F, _P, _SZ, _P]),
+    "readme_offload_stats": (_I32, [_P, _P, _P, _P]),
+    "readme_offload_destroy": (None, [_P]),
     "readme_ungroup": (_I32, [_I32, _I64, _I64, _P, _P, _P, _P]),
     "readme_moe_ffn_stack_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
     "readme_moe_ffn_stack": (_I32, [_I64, _I64, _I32, _I64, _I32, _P, _P, _P, _F, _P,
@@ -451,6 +455,51 @@ def readme_cache_simulate(refs, capacity: int, policy: str, seed: int = 0):
           hits.ctypes.data_as(ctypes.c_void_p), evicted.ctypes.data_as(ctypes.c_void_p),
           ctypes.byref(nh))
     return hits[:n].astype(bool).tolist(), evicted[:n].tolist(), nh.value
+
+
+class Offload:
+    """Expert-offload executor (readme_offload_*): packed layers in pinned host
+    memory, `slots` device slots, copies one layer ahead on its own stream."""
+
+    def __init__(self, packed_layers, E, d, I, slots, policy="belady"):
+        arr = (ctypes.c_void_p * len(packed_layers))(*[p.data_ptr() for p in packed_layers])
+        h = ctypes.c_void_p()
+        _call("readme_offload_create", E, d, I, len(packed_layers), slots,
+              README_CACHE_POLICIES[policy], arr, ctypes.byref(h),
+              _stream(packed_layers[0].device))
+        self.h, self.E, self.d, self.I, self.L = h, E, d, I, len(packed_layers)
+
+    def stack(self, x_resid_grouped, offsets, counts, next_counts=None, rms_eps=1e-5,
+              workspace=None):
+        import numpy as np
+        T = x_resid_grouped.shape[0]
+        ws = readme_moe_ffn_stack_workspace_bytes(T, self.d, self.I)
+        if workspace is None:
+            workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=x_resid_grouped.device)
+        _dev(x_resid_grouped, offsets, workspace)
+        c = np.ascontiguousarray(counts, dtype=np.int32)
+        nc = None if next_counts is None else np.ascontiguousarray(next_counts, dtype=np.int32)
+        _call("readme_offload_stack", self.h, T, _p(offsets), c.ctypes.data_as(ctypes.c_void_p),
+              None if nc is None else nc.ctypes.data_as(ctypes.c_void_p), _p(x_resid_grouped),
+              rms_eps, _p(workspace), workspace.numel() * workspace.element_size(),
+              _stream(x_resid_grouped.device))
+        return x_resid_grouped
+
+    def stats(self):
+        h, m, b = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+        _call("readme_offload_stats", self.h, ctypes.byref(h), ctypes.byref(m), ctypes.byref(b))
+        return h.value, m.value, b.value
+
+    def close(self):
+        if self.h:
+            load().readme_offload_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def readme_ungroup(y_grouped, inv_perm, y=None):

@@ -24,6 +24,10 @@ readme_status check_ffn_shape(readme_dtype dt, int64_t T, int64_t d, int32_t E, 
     return README_OK;
 }
 
+}  // namespace
+
+namespace readme {
+
 GemmArgs gate_up_args(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I,
                       const void* xg, const int32_t* offsets, const void* packed, void* h) {
     const int64_t Ip = padded_I(I);
@@ -103,7 +107,8 @@ readme_status ffn_permanent(readme_dtype dt, int64_t T, int64_t d, int32_t E, in
     return hip_status(err);
 }
 
-}  // namespace
+}  // namespace readme
+
 
 extern "C" {
 

@@ -296,7 +296,8 @@ __device__ __forceinline__ WeightSteps weight_steps(const GemmArgs& g, int e, in
     const int segs = SEG && g.k_segs > 1 ? g.k_segs : 1;
     w.B0 = reinterpret_cast<const char*>(g.B);
     w.estride = g.b_expert_stride * esz;
-    w.own = w.B0 + (int64_t)e * w.estride;
+    const int we = g.b_index && e < g.E ? g.b_index[e] : e;  // slot of expert e, if cached
+    w.own = w.B0 + (int64_t)we * w.estride;
     w.step_bytes = step_bytes;
     w.nks = (uint32_t)(g.K / segs / bk);
     w.mult = segs > 1 ? (uint32_t)(((1ull << 32) + w.nks - 1) / w.nks) : 0u;

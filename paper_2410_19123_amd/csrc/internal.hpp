@@ -41,6 +41,9 @@ struct GemmArgs {
     int shared_groups;
     int64_t shared_col_stride;  // elements
     int k_segs;
+    // b_index (device, [E], nullable): expert e's weights are weight index
+    // b_index[e] instead of e (a cache of expert slots).
+    const int32_t* b_index;
     int n_tiles, m_tiles_max; // filled by the launcher
 };
 
@@ -61,6 +64,11 @@ hipError_t launch_pack_slots(readme_dtype dt, int64_t E_all, int64_t e0, int64_t
                              int64_t wd_expert_stride, int64_t wd_row_stride, void* packed,
                              hipStream_t s);
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s);
+// Arguments of the two FFN GEMMs over a packed expert buffer (abi.hip).
+GemmArgs gate_up_args(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I,
+                      const void* xg, const int32_t* offsets, const void* packed, void* h);
+GemmArgs down_args(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I, const void* h,
+                   const int32_t* offsets, const void* packed, void* y);
 bool set_gemm_tile(int tile);
 hipError_t launch_topk(int64_t T, int E, int K, const float* logits, int32_t* ids, float* weights,
                        hipStream_t s);

@@ -61,6 +61,8 @@ class Workload:
     K: int = 1
     batching: str = ""    # "alg1" | "fifo": batches drawn from a pool of waiting requests
     pool: int = 0         # waiting decode requests the batches are drawn from
+    offload_slots: int = 0  # >0: weights in host memory, a device cache of this many slots
+    policy: str = ""      # the cache's replacement rule: "belady" | "lru"
     layers: int = 1
     router: bool = True
     bias: str = "none"    # "none" | "zipf1" | "skew40_zipf1.2"
@@ -102,6 +104,19 @@ WORKLOADS = {
         description="serving loop: 64-token decode batches taken first-come "
                     "first-served from 1024 waiting requests, 32 stacked "
                     "Llama-7B-shaped MoE layers"),
+    "llama7b_decode8_offload_belady": Workload(
+        "llama7b_decode8_offload_belady", T=64, d=4096, E=8, I=1376, dtype="bf16",
+        layers=8, router=False, batching="fifo", pool=1024, offload_slots=24,
+        policy="belady",
+        description="serving loop with expert offload: 64-token first-come "
+                    "first-served decode batches through 8 Llama-7B-shaped MoE "
+                    "layers whose experts live in host memory, 24 device slots "
+                    "of the 64 (layer, expert) pairs, Belady replacement"),
+    "llama7b_decode8_offload_lru": Workload(
+        "llama7b_decode8_offload_lru", T=64, d=4096, E=8, I=1376, dtype="bf16",
+        layers=8, router=False, batching="fifo", pool=1024, offload_slots=24,
+        policy="lru",
+        description="as llama7b_decode8_offload_belady with LRU replacement"),
     "prefill_skew16": Workload(
         "prefill_skew16", T=16384, d=4096, E=16, I=688, dtype="bf16",
         bias="skew40_zipf1.2",

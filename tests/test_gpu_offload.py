@@ -1,0 +1,81 @@
+"""The expert-offload executor (Sec. 4.1) through the C ABI: the layer stack
+computed with weights fetched into a small device cache of (layer, expert)
+slots equals the resident stack bit for bit, step after step, under both
+replacement policies; its counters add up."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2410_19123_amd import workloads as wl
+
+from . import _util as U
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    from paper_2410_19123_amd import _lib
+    _lib.load()
+    return _lib
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+@pytest.mark.parametrize("policy", ["belady", "lru"])
+def test_offload_stack_equals_resident(L, policy):
+    w = wl.Workload("t", T=48, d=256, E=6, I=160, dtype="bf16", layers=4)
+    _say("offload", policy)
+    layers = [L.readme_pack_experts(*U.weights_to_dev(*wl.make_experts(w, 50, layer=l)))
+              for l in range(w.layers)]
+    slots = 8
+    ex = L.Offload(layers, w.E, w.d, w.I, slots, policy)
+    rng = np.random.default_rng(50)
+    steps = 7
+    # each step routes the tokens to 1..4 experts
+    plans = []
+    for _ in range(steps):
+        k = int(rng.integers(1, 5))
+        experts = rng.choice(w.E, size=k, replace=False)
+        plans.append(rng.choice(experts, size=w.T).astype(np.int32))
+    slot_bytes = 3 * L.readme_padded_intermediate(w.I) * w.d * 2
+    refs = 0
+    x0 = np.random.default_rng(51).standard_normal((w.T, w.d)).astype(np.float32)
+    try:
+        for st in range(steps):
+            ids = U.to_dev(plans[st])
+            counts, offs, perm, inv, xg = L.readme_group_by_expert(ids, w.E, x=U.to_dev(x0))
+            c = np.bincount(plans[st], minlength=w.E)
+            nxt = np.bincount(plans[st + 1], minlength=w.E) if st + 1 < steps else None
+            xa, xb = xg.clone(), xg.clone()
+            L.readme_moe_ffn_stack(xa, offs, layers, w.E, w.I)
+            ex.stack(xb, offs, c, nxt)
+            torch.cuda.synchronize()
+            assert (U.from_dev(xa) == U.from_dev(xb)).all(), st
+            refs += w.layers * int((c > 0).sum())
+        hits, misses, nbytes = ex.stats()
+        assert hits + misses == refs
+        assert nbytes == misses * slot_bytes
+        assert misses >= min(refs, slots)  # every key is loaded once at least
+    finally:
+        ex.close()
+
+
+def test_offload_needs_two_layers_of_slots(L):
+    w = wl.Workload("t", T=32, d=128, E=4, I=64, dtype="bf16", layers=2)
+    layers = [L.readme_pack_experts(*U.weights_to_dev(*wl.make_experts(w, 60, layer=l)))
+              for l in range(w.layers)]
+    ex = L.Offload(layers, w.E, w.d, w.I, 5, "belady")
+    try:
+        ids = U.to_dev(np.arange(w.T, dtype=np.int32) % 3)       # 3 experts need 6 slots
+        counts, offs, perm, inv, xg = L.readme_group_by_expert(
+            ids, w.E, x=U.to_dev(np.ones((w.T, w.d), np.float32)))
+        with pytest.raises(L.ReadmeError) as e:
+            ex.stack(xg, offs, np.bincount(U.from_dev(ids), minlength=w.E))
+        assert e.value.status == 2
+    finally:
+        ex.close()
