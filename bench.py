@@ -325,8 +325,8 @@ TRAFFIC_SOURCES = ["csrc/gemm_kernels.hpp", "csrc/gemm.hip", "csrc/gemm_bf16_gat
                    "csrc/common.hpp", "csrc/internal.hpp", "csrc/pack.hip", "workloads.py"]
 TRAFFIC = {
     # workload: (sources sha256, read bytes, written bytes) per gate/up launch
-    "llama7b_layer": ("9e2a1d4a8d343db4c2a2f9ae1b8cadf39c681f3e76cfdd11fd471869c670073e",
-                      234303263, 5767168),
+    "llama7b_layer": ("5b74149d00227f79634526f6d6f1a4ad68935db23fcf77764f38c6a20f105755",
+                      234307270, 5767168),
 }
 
 
