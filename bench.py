@@ -246,8 +246,18 @@ class Path:
             w.T, w.E, P(ids), P(self.counts), P(self.offsets), P(self.perm), P(self.inv),
             0, w.d, P(self.x32), P(self.xres), self.stream), "group")
 
-    def stack(self):
+    def stack(self, k=0):
         P, w = self.P, self.w
+        if w.batching:
+            # The scheduler formed the batch, so its expert counts are known on
+            # the host: the library picks tiles for the actual split.
+            n = self.sched.shape[0]
+            cnt = np.ascontiguousarray(np.bincount(self.sched[k % n], minlength=w.E), np.int32)
+            self._ok(self.lib.readme_moe_ffn_stack_counts(
+                w.T, w.d, w.E, w.I, w.layers, ctypes.cast(self.layer_ptrs, ctypes.c_void_p),
+                P(self.offsets), cnt.ctypes.data_as(ctypes.c_void_p), P(self.xres),
+                ctypes.c_float(1e-5), P(self.ws), self.ws.numel(), self.stream), "stack")
+            return
         self._ok(self.lib.readme_moe_ffn_stack(
             w.T, w.d, w.E, w.I, w.layers, ctypes.cast(self.layer_ptrs, ctypes.c_void_p),
             P(self.offsets), P(self.xres), ctypes.c_float(1e-5), P(self.ws),
@@ -298,7 +308,7 @@ class Path:
         """(name, call) of one step, in path order; k picks the weight copy.
         fused: the row gather and the ungroup ride in the two GEMMs."""
         if self.w.layers > 1:
-            stack = (lambda: self.offload_stack(k)) if self.ex else self.stack
+            stack = (lambda: self.offload_stack(k)) if self.ex else (lambda: self.stack(k))
             return [("route", self.route), ("group", lambda: self.group_resid(k)),
                     ("stack", stack), ("ungroup", self.ungroup_resid)]
         if self.w.K > 1:

@@ -166,7 +166,7 @@ int64_t readme_padded_intermediate(int64_t I);
  *   weights streamed straight into registers (bf16; fp32 runs tile 6):
  *     12 = 128x256, 13 = 64x256, 14 = 32x256, 15 = 32x128 (deep pipeline),
  *     16 = 256x256, 19 = 128x256 (5 stages), 20 = 128x256 (6 stages),
- *     21 = 192x256 (3 stages), 22 = 192x256 (2 stages)
+ *     21 = 192x256 (3 stages), 22 = 192x256 (2 stages), 23 = 32x64
  *   (rows of tokens x columns of outputs)
  * Results do not depend on the tile beyond fp32 summation order.  Returns
  * README_ERR_ARG for any other value.  Not synchronised with calls in
@@ -512,6 +512,22 @@ readme_status readme_moe_ffn_stack(int64_t T, int64_t d, int32_t E,
                                    float *x_resid_grouped, float rms_eps,
                                    void *workspace, size_t workspace_bytes,
                                    void *stream);
+
+/*
+ * readme_moe_ffn_stack_counts -- readme_moe_ffn_stack for a caller that knows
+ * the batch's token counts per expert on the host (a scheduler that formed
+ * the batch, e.g. by readme_expert_batch): counts [E] (host) must be the
+ * counts of `offsets`.  The tiles are then chosen for the actual split (a
+ * batch on few experts gets narrower tiles, so more workgroups stream the
+ * weights); results are bit-identical to readme_moe_ffn_stack.
+ * README_ERR_ARG for a NULL or negative count.
+ */
+readme_status readme_moe_ffn_stack_counts(int64_t T, int64_t d, int32_t E, int64_t I,
+                                          int32_t L, const void *const *packed_per_layer,
+                                          const int32_t *offsets, const int32_t *counts,
+                                          float *x_resid_grouped, float rms_eps,
+                                          void *workspace, size_t workspace_bytes,
+                                          void *stream);
 
 #ifdef __cplusplus
 }

@@ -72,6 +72,8 @@ SIGNATURES = {
     "readme_moe_ffn_stack_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
     "readme_moe_ffn_stack": (_I32, [_I64, _I64, _I32, _I64, _I32, _P, _P, _P, _F, _P,
                                     _SZ, _P]),
+    "readme_moe_ffn_stack_counts": (_I32, [_I64, _I64, _I32, _I64, _I32, _P, _P, _P, _P, _F,
+                                           _P, _SZ, _P]),
 }
 
 _lib = None
@@ -518,8 +520,9 @@ def readme_moe_ffn_stack_workspace_bytes(T, d, I) -> int:
 
 
 def readme_moe_ffn_stack(x_resid_grouped, offsets, packed_layers, E, I, rms_eps=1e-5,
-                         workspace=None):
-    """Run len(packed_layers) pre-norm residual MoE layers in place on x (fp32)."""
+                         workspace=None, counts=None):
+    """Run len(packed_layers) pre-norm residual MoE layers in place on x (fp32).
+    counts (host, [E]): the batch's token counts, for the tile choice."""
     T, d = x_resid_grouped.shape
     if x_resid_grouped.dtype != torch.float32:
         raise ValueError("the residual stream is fp32")
@@ -529,9 +532,15 @@ def readme_moe_ffn_stack(x_resid_grouped, offsets, packed_layers, E, I, rms_eps=
         workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=x_resid_grouped.device)
     _dev(x_resid_grouped, offsets, workspace, *packed_layers)
     ptrs = (ctypes.c_void_p * max(L, 1))(*[p.data_ptr() for p in packed_layers])
-    _call("readme_moe_ffn_stack", T, d, E, I, L, ctypes.cast(ptrs, ctypes.c_void_p),
-          _p(offsets), _p(x_resid_grouped), float(rms_eps), _p(workspace),
-          workspace.numel() * workspace.element_size(), _stream(x_resid_grouped.device))
+    if counts is None:
+        _call("readme_moe_ffn_stack", T, d, E, I, L, ctypes.cast(ptrs, ctypes.c_void_p),
+              _p(offsets), _p(x_resid_grouped), float(rms_eps), _p(workspace),
+              workspace.numel() * workspace.element_size(), _stream(x_resid_grouped.device))
+    else:
+        c, pc = _host_i32(counts)
+        _call("readme_moe_ffn_stack_counts", T, d, E, I, L, ctypes.cast(ptrs, ctypes.c_void_p),
+              _p(offsets), pc, _p(x_resid_grouped), float(rms_eps), _p(workspace),
+              workspace.numel() * workspace.element_size(), _stream(x_resid_grouped.device))
     return x_resid_grouped
 
 

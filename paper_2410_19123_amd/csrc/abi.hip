@@ -442,10 +442,12 @@ size_t readme_moe_ffn_stack_workspace_bytes(int64_t T, int64_t d, int64_t I) {
     return (size_t)T * d * 2 + (size_t)T * padded_I(I) * 2;
 }
 
-readme_status readme_moe_ffn_stack(int64_t T, int64_t d, int32_t E, int64_t I, int32_t L,
-                                   const void* const* packed_per_layer, const int32_t* offsets,
-                                   float* x_resid_grouped, float rms_eps, void* workspace,
-                                   size_t workspace_bytes, void* stream) {
+namespace {
+
+readme_status stack_impl(int64_t T, int64_t d, int32_t E, int64_t I, int32_t L,
+                         const void* const* packed_per_layer, const int32_t* offsets,
+                         const int32_t* counts, float* x_resid_grouped, float rms_eps,
+                         void* workspace, size_t workspace_bytes, void* stream) {
     readme_status st = check_ffn_shape(README_BF16, T, d, E, I);
     if (st != README_OK) return st;
     if (L < 0 || !(rms_eps >= 0.0f)) return README_ERR_ARG;
@@ -456,6 +458,13 @@ readme_status readme_moe_ffn_stack(int64_t T, int64_t d, int32_t E, int64_t I, i
         if (!packed_per_layer[l] || !a16(packed_per_layer[l])) return README_ERR_ARG;
     if (workspace_bytes < readme_moe_ffn_stack_workspace_bytes(T, d, I))
         return README_ERR_WORKSPACE;
+    int m32 = 0;
+    if (counts) {
+        for (int32_t e = 0; e < E; ++e) {
+            if (counts[e] < 0) return README_ERR_ARG;
+            m32 += (counts[e] + 31) / 32;
+        }
+    }
     hipStream_t s = as_stream(stream);
     uint16_t* xn = reinterpret_cast<uint16_t*>(workspace);
     uint16_t* h = xn + T * d;
@@ -463,14 +472,36 @@ readme_status readme_moe_ffn_stack(int64_t T, int64_t d, int32_t E, int64_t I, i
         hipError_t err = launch_rms_to_bf16(T, d, x_resid_grouped, offsets, E, rms_eps, xn, s);
         if (err != hipSuccess) return README_ERR_HIP;
         GemmArgs gu = gate_up_args(README_BF16, T, d, E, I, xn, offsets, packed_per_layer[l], h);
+        gu.m_tiles32 = m32;
         err = launch_grouped_gemm(false, EPI_GATE_UP_SILU, gu, s);
         if (err != hipSuccess) return README_ERR_HIP;
         GemmArgs dn = down_args(README_BF16, T, d, E, I, h, offsets, packed_per_layer[l],
                                 x_resid_grouped);
+        dn.m_tiles32 = m32;
         err = launch_grouped_gemm(false, EPI_RESID_ADD, dn, s);
         if (err != hipSuccess) return README_ERR_HIP;
     }
     return README_OK;
+}
+
+}  // namespace
+
+readme_status readme_moe_ffn_stack(int64_t T, int64_t d, int32_t E, int64_t I, int32_t L,
+                                   const void* const* packed_per_layer, const int32_t* offsets,
+                                   float* x_resid_grouped, float rms_eps, void* workspace,
+                                   size_t workspace_bytes, void* stream) {
+    return stack_impl(T, d, E, I, L, packed_per_layer, offsets, nullptr, x_resid_grouped,
+                      rms_eps, workspace, workspace_bytes, stream);
+}
+
+readme_status readme_moe_ffn_stack_counts(int64_t T, int64_t d, int32_t E, int64_t I, int32_t L,
+                                          const void* const* packed_per_layer,
+                                          const int32_t* offsets, const int32_t* counts,
+                                          float* x_resid_grouped, float rms_eps, void* workspace,
+                                          size_t workspace_bytes, void* stream) {
+    if (!counts) return README_ERR_ARG;
+    return stack_impl(T, d, E, I, L, packed_per_layer, offsets, counts, x_resid_grouped,
+                      rms_eps, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

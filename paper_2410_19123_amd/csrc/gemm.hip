@@ -33,7 +33,14 @@ static int tile_by_shape(bool f32, bool gate_up, const GemmArgs& g) {
         if (per_expert >= (gate_up ? 768 : 192)) return TILE_256x256;
         return per_expert >= 96 && !gate_up ? TILE_128x256 : TILE_32x128;
     }
-    if (per_expert < 96) return TILE_BD_32x128;
+    if (per_expert < 96) {
+        // Decode: 32-row tiles.  When the caller's counts show few of them
+        // (tokens concentrated on few experts), halve the tile width so that
+        // twice as many workgroups stream the weights.
+        if (g.m_tiles32 > 0 && (int64_t)g.m_tiles32 * ceil_div(g.N, 128) < 128)
+            return TILE_BD_32x64;
+        return TILE_BD_32x128;
+    }
     if (gate_up) {
         if (per_expert >= 768) return g.K >= 8192 ? TILE_BD_192x256 : TILE_256x256;
         // 128-row tiles while their estimated count (half a tile of padding

@@ -859,7 +859,8 @@ enum TileCfg {
     TILE_BD_128x256_S6 = 20,  // as 12, 6 K-steps in flight
     TILE_BD_192x256 = 21,     // 4 waves of 192x64, 3 K-steps
     TILE_BD_192x256_S2 = 22,  // 4 waves of 192x64, 2 K-steps
-    TILE_LAST = TILE_BD_192x256_S2,
+    TILE_BD_32x64 = 23,       // 1 wave of 32x64, 6 K-steps
+    TILE_LAST = TILE_BD_32x64,
 };
 
 // Launches one tile configuration (instantiated per element type and
@@ -892,6 +893,7 @@ hipError_t launch_tile(int tile, GemmArgs g, hipStream_t s) {
             case TILE_BD_128x256_S6: return launch_bd<128, 4, 2, 6, F32, EPI>(g, s);
             case TILE_BD_192x256: return launch_bd<192, 4, 2, 3, F32, EPI>(g, s);
             case TILE_BD_192x256_S2: return launch_bd<192, 4, 2, 2, F32, EPI>(g, s);
+            case TILE_BD_32x64: return launch_bd<32, 1, 2, 6, F32, EPI>(g, s);
             default: break;
         }
     }

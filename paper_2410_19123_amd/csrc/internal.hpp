@@ -44,6 +44,9 @@ struct GemmArgs {
     // b_index (device, [E], nullable): expert e's weights are weight index
     // b_index[e] instead of e (a cache of expert slots).
     const int32_t* b_index;
+    // m_tiles32 > 0: sum over experts of ceil(rows_e / 32), from token counts
+    // the caller knows on the host (the tile choice then sees the split).
+    int m_tiles32;
     int n_tiles, m_tiles_max; // filled by the launcher
 };
 

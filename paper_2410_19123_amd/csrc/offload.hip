@@ -276,6 +276,8 @@ readme_status readme_offload_stack(readme_offload* ex, int64_t T, const int32_t*
 
     uint16_t* xn = reinterpret_cast<uint16_t*>(workspace);
     uint16_t* h = xn + T * ex->d;
+    int m32 = 0;  // 32-row tiles of the batch, for the tile choice
+    for (int e = 0; e < E; ++e) m32 += (counts[e] + 31) / 32;
     const int64_t slot_elems = (int64_t)(ex->slot_bytes / 2);
     for (int l = 0; l < L; ++l) {
         if (l + 1 < L && !issue(l + 1)) return README_ERR_HIP;
@@ -284,12 +286,14 @@ readme_status readme_offload_stack(readme_offload* ex, int64_t T, const int32_t*
         GemmArgs gu = gate_up_args(README_BF16, T, ex->d, E, ex->I, xn, offsets, ex->dev_slots, h);
         gu.b_expert_stride = slot_elems;
         gu.b_index = dev_table + (size_t)l * E;
+        gu.m_tiles32 = m32;
         if (err == hipSuccess) err = launch_grouped_gemm(false, EPI_GATE_UP_SILU, gu, s);
         GemmArgs dn = down_args(README_BF16, T, ex->d, E, ex->I, h, offsets, ex->dev_slots,
                                 x_resid_grouped);
         dn.B = ex->dev_slots + ex->gu_bytes;
         dn.b_expert_stride = slot_elems;
         dn.b_index = dev_table + (size_t)l * E;
+        dn.m_tiles32 = m32;
         if (err == hipSuccess) err = launch_grouped_gemm(false, EPI_RESID_ADD, dn, s);
         if (err != hipSuccess || hipEventRecord(ex->done[l], s) != hipSuccess)
             return README_ERR_HIP;

@@ -146,3 +146,13 @@ def test_topk_argument_errors(lib):
     assert c(1, 16, 4, 2, FAKE, FAKE, FAKE, None) == 2     # 8-byte rows
     assert c(1, 16, 64, 0, FAKE, FAKE, FAKE, None) == 1
     assert c(1, 16, 64, 2, FAKE, None, FAKE, None) == 1
+
+
+def test_stack_counts_argument_errors(lib):
+    s = lib.readme_moe_ffn_stack_counts
+    arr = (ctypes.c_void_p * 1)(4096)
+    assert s(64, 4096, 8, 1376, 1, arr, FAKE, None, FAKE, ctypes.c_float(1e-5), FAKE, 1 << 40,
+             None) == 1                                          # no counts
+    neg = (ctypes.c_int32 * 8)(1, 2, -1, 0, 0, 0, 0, 0)
+    assert s(64, 4096, 8, 1376, 1, arr, FAKE, neg, FAKE, ctypes.c_float(1e-5), FAKE, 1 << 40,
+             None) == 1                                          # negative count

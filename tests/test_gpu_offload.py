@@ -79,3 +79,25 @@ def test_offload_needs_two_layers_of_slots(L):
         assert e.value.status == 2
     finally:
         ex.close()
+
+
+@pytest.mark.parametrize("concentrated", [True, False])
+def test_stack_with_counts_equals_plain_stack(L, concentrated):
+    """Host counts only change the tile choice (narrower tiles for a batch on
+    few experts); every tile accumulates K in the same order, so the stack
+    gives the same bits."""
+    w = wl.Workload("t", T=64, d=512, E=8, I=256, dtype="bf16", layers=3)
+    layers = [L.readme_pack_experts(*U.weights_to_dev(*wl.make_experts(w, 70, layer=l)))
+              for l in range(w.layers)]
+    rng = np.random.default_rng(70)
+    ids_h = (np.full(w.T, 3, np.int32) if concentrated
+             else rng.integers(0, w.E, size=w.T).astype(np.int32))
+    x0 = rng.standard_normal((w.T, w.d)).astype(np.float32)
+    counts, offs, perm, inv, xg = L.readme_group_by_expert(U.to_dev(ids_h), w.E,
+                                                           x=U.to_dev(x0))
+    xa, xb = xg.clone(), xg.clone()
+    L.readme_moe_ffn_stack(xa, offs, layers, w.E, w.I)
+    L.readme_moe_ffn_stack(xb, offs, layers, w.E, w.I,
+                           counts=np.bincount(ids_h, minlength=w.E))
+    torch.cuda.synchronize()
+    assert (U.from_dev(xa) == U.from_dev(xb)).all()
