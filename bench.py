@@ -327,7 +327,7 @@ class Path:
 # HBM traffic of the dominant kernel, per launch, from two rocprofv3 --pmc runs of
 # this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each scaled by what
 # the same counter reads for a plain 1 GiB device copy in the same run (--copy-probe:
-# FETCH_SIZE reads 524307 KiB for it, so reads scale by 1.99993; WRITE_SIZE reads
+# FETCH_SIZE reads about 524,310 KiB for it, so reads scale by about 1.9999; WRITE_SIZE reads
 # exactly 1 GiB, factor 1).  Valid only for the sources the counters were taken
 # with: the entry carries their sha256 and is dropped (traffic null) once any of
 # them changes.
