@@ -468,8 +468,8 @@ def main():
 
     def step(i, mode):
         """mode None: no events; "dom": an event pair around the dominant
-        kernel only (the timed region, so events add little to the step);
-        "all": an event before every call (the per-call breakdown pass)."""
+        kernel only (the timed region); "all": an event before every call
+        (the per-call breakdown pass)."""
         k = i % ncopy
         marks = []
         for n, fn in path.calls(k, fused):
@@ -496,8 +496,12 @@ def main():
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     start.record()
+    # The dominant kernel's event pair goes on every 8th step of the timed
+    # region: a timing event pair costs ~4.5 us of a ~140 us step (measured
+    # with and without it), so sampling keeps the step time honest while the
+    # launch average still spans the whole region.
     for i in range(K):
-        step(W + i, "dom")
+        step(W + i, "dom" if i % 8 == 0 else None)
     stop.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0

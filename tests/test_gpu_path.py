@@ -94,7 +94,11 @@ def _ids_case(kind, T, E, seed):
     ("uniform", 1, 1), ("uniform", 63, 4), ("uniform", 65, 4), ("uniform", 1024, 8),
     ("uniform", 1025, 8), ("uniform", 16384, 16), ("uniform", 5000, 256),
     ("one_expert", 3000, 8), ("empty_ends", 2048, 8), ("invalid", 2500, 7),
-    ("local", 4096, 8), ("uniform", 40000, 3), ("uniform", 0, 4)])
+    ("local", 4096, 8), ("uniform", 40000, 3), ("uniform", 0, 4),
+    # many 1024-id rounds with many experts, invalid ids among 200 experts,
+    # and sizes on both sides of 16 rounds
+    ("uniform", 16384, 256), ("invalid", 9000, 200), ("local", 16384, 8),
+    ("uniform", 16385, 8), ("empty_ends", 16383, 64)])
 def test_group_bit_exact(L, oracle_mod, kind, T, E):
     _say("group", kind, T, E)
     ids = _ids_case(kind, T, E, seed=T + E)
