@@ -275,6 +275,26 @@ def test_decode_stack_teacher_forced(L, oracle_mod):
     assert (U.from_dev(y) == U.from_dev(xa)[U.from_dev(inv)]).all()
 
 
+@pytest.mark.parametrize("d", [320, 4160, 8256])
+def test_stack_layer_norm_widths(L, oracle_mod, d):
+    """One stacked layer at model widths where the pre-norm holds a row in
+    registers as up to 4 (d = 320) or 8 (d = 4160) vectors per thread, or
+    reads it twice (d = 8256); ragged experts, one of them empty."""
+    _say("stack width", d)
+    w = wl.Workload("t", T=70, d=d, E=4, I=96, dtype="bf16")
+    x = wl.make_x(w, d)
+    counts = np.array([33, 0, 30, 7], np.int32)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    host = wl.make_experts(w, d)
+    packed = L.readme_pack_experts(*U.weights_to_dev(*host))
+    xr = U.to_dev(wl.bf16_bits_to_f32(x)).float()
+    x_in = U.from_dev(xr).copy()
+    L.readme_moe_ffn_stack(xr, U.to_dev(offsets), [packed], w.E, w.I)
+    torch.cuda.synchronize()
+    delta = U.from_dev(xr).astype(np.float64) - x_in.astype(np.float64)
+    U.close(delta, oracle_mod.layer(x_in, offsets, *host, eps=1e-5), f"d {d}")
+
+
 # ------------------------------------------------------ every tile config
 @pytest.mark.parametrize("tile", list(range(1, 24)))
 def test_every_gemm_tile_matches_oracle(L, oracle_mod, tile):
