@@ -362,6 +362,120 @@ __global__ __launch_bounds__(512) void k_route_lds(int64_t T, int64_t d, int E, 
     }
 }
 
+// bf16 variant for one token per wave: the router matrix is staged in LDS
+// as fp32, in two planes (elements 0-3 and 4-7 of each 8-element chunk, so
+// consecutive lanes still read consecutive 16 bytes), converted once per
+// workgroup instead of once per token.  Same summation order as k_route.
+template <int CPL, int LDS_BYTES, int EB>
+__global__ __launch_bounds__(512) void k_route_lds_f32w(int64_t T, int64_t d, int E, int tb,
+                                                        const void* __restrict__ x,
+                                                        const void* __restrict__ wr,
+                                                        const float* __restrict__ bias,
+                                                        int32_t* __restrict__ ids,
+                                                        float* __restrict__ logits) {
+    constexpr int PLANE = LDS_BYTES / 32;  // float4 per plane
+    __shared__ float4 wl[2][PLANE];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int nchunks = (int)(d / 8);
+    const uint4* xq = reinterpret_cast<const uint4*>(x);
+    const int64_t tb0 = (int64_t)blockIdx.x * tb;
+    uint4 xr[CPL];
+    auto load_x = [&](int64_t t) {
+        const int64_t row = (t < T ? t : T - 1) * nchunks;
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            const int c = lane + 64 * j;
+            xr[j] = c < nchunks ? xq[row + c] : make_uint4(0, 0, 0, 0);
+        }
+    };
+    // The first token row is requested before the router matrix is staged.
+    if (wave < tb && tb0 + wave < T) load_x(tb0 + wave);
+    {
+        const uint4* wq = reinterpret_cast<const uint4*>(wr);
+        const int n = E * nchunks;
+        constexpr int PER = PLANE / 512;
+        constexpr int BATCH = PER < 8 ? PER : 8;
+#pragma unroll
+        for (int k0 = 0; k0 < PER; k0 += BATCH) {
+            uint4 tmp[BATCH];
+#pragma unroll
+            for (int k = 0; k < BATCH; ++k) {
+                const int i = (int)threadIdx.x + 512 * (k0 + k);
+                tmp[k] = i < n ? wq[i] : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int k = 0; k < BATCH; ++k) {
+                const int i = (int)threadIdx.x + 512 * (k0 + k);
+                if (i < n) {
+                    float v[8];
+                    Chunk<8>::unpack(tmp[k], v);
+                    wl[0][i] = make_float4(v[0], v[1], v[2], v[3]);
+                    wl[1][i] = make_float4(v[4], v[5], v[6], v[7]);
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    for (int g = wave; g < tb; g += 8) {
+        const int64_t t = tb0 + g;
+        if (t >= T) break;
+        if (g != wave) load_x(t);
+        float best = 0.0f;
+        int bid = 0;
+        for (int e0 = 0; e0 < E; e0 += EB) {
+            float acc[EB];
+#pragma unroll
+            for (int b = 0; b < EB; ++b) acc[b] = 0.0f;
+#pragma unroll
+            for (int j = 0; j < CPL; ++j) {
+                const int c = lane + 64 * j;
+                if (c >= nchunks) break;
+                float xv[8];
+                Chunk<8>::unpack(xr[j], xv);
+#pragma unroll
+                for (int b = 0; b < EB; ++b) {
+                    if (e0 + b >= E) break;
+                    const float4 w0 = wl[0][(e0 + b) * nchunks + c];
+                    const float4 w1 = wl[1][(e0 + b) * nchunks + c];
+                    acc[b] = __builtin_fmaf(xv[0], w0.x, acc[b]);
+                    acc[b] = __builtin_fmaf(xv[1], w0.y, acc[b]);
+                    acc[b] = __builtin_fmaf(xv[2], w0.z, acc[b]);
+                    acc[b] = __builtin_fmaf(xv[3], w0.w, acc[b]);
+                    acc[b] = __builtin_fmaf(xv[4], w1.x, acc[b]);
+                    acc[b] = __builtin_fmaf(xv[5], w1.y, acc[b]);
+                    acc[b] = __builtin_fmaf(xv[6], w1.z, acc[b]);
+                    acc[b] = __builtin_fmaf(xv[7], w1.w, acc[b]);
+                }
+            }
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1)
+#pragma unroll
+                for (int b = 0; b < EB; ++b) {
+                    const float o = __shfl_down(acc[b], off, 64);
+                    acc[b] = acc[b] + o;
+                }
+#pragma unroll
+            for (int b = 0; b < EB; ++b) {
+                const int e = e0 + b;
+                if (e >= E) break;
+                float logit = __shfl(acc[b], 0, 64);
+                if (bias) logit = logit + bias[e];
+                if (logits && lane == 0) logits[t * E + e] = logit;
+                if (e == 0) {
+                    best = logit;
+                    bid = 0;
+                } else if (logit > best) {
+                    best = logit;
+                    bid = e;
+                }
+            }
+        }
+        if (lane == 0) ids[t] = bid;
+    }
+}
+
 template <int R, int CPL, int W, int LDS_BYTES>
 static hipError_t launch_route_lds_r(int64_t T, int64_t d, int E, const void* x, const void* w,
                                      const float* bias, int32_t* ids, float* logits,
@@ -386,6 +500,21 @@ static hipError_t launch_route_lds_r(int64_t T, int64_t d, int E, const void* x,
 
 // R tokens per wave group: as many as the token rows' registers allow with
 // two waves per SIMD (no spills).
+// One token per wave with the router as fp32 planes (bf16, E * d * 4 <= 128 KB).
+template <int CPL>
+static hipError_t launch_route_f32w(int64_t T, int64_t d, int E, const void* x, const void* w,
+                                    const float* bias, int32_t* ids, float* logits,
+                                    hipStream_t s) {
+    int64_t tb = ceil_div(T, 256);
+    tb = tb < 8 ? 8 : (tb > 128 ? 128 : tb);
+    const dim3 grid((unsigned)ceil_div(T, tb)), block(512);
+    if ((int64_t)E * d * 4 <= 65536)
+        k_route_lds_f32w<CPL, 65536, 4><<<grid, block, 0, s>>>(T, d, E, (int)tb, x, w, bias, ids, logits);
+    else
+        k_route_lds_f32w<CPL, 131072, 4><<<grid, block, 0, s>>>(T, d, E, (int)tb, x, w, bias, ids, logits);
+    return hipGetLastError();
+}
+
 template <int W, int LDS_BYTES>
 static hipError_t launch_route_lds(int cpl, int64_t T, int64_t d, int E, const void* x,
                                    const void* w, const float* bias, int32_t* ids, float* logits,
@@ -434,6 +563,18 @@ hipError_t launch_route(readme_dtype dt, int64_t T, int64_t d, int E, const void
         while (64 * cpl < nchunks) cpl *= 2;
         // Router matrix in LDS when it fits (64 KB, or 128 KB for many tokens).
         const int64_t wbytes = (int64_t)E * d * (dt == README_BF16 ? 2 : 4);
+        // bf16 with one token per wave: router unpacked to fp32 once per
+        // workgroup when it fits (measured at T = 2048, d = 4096, E = 8:
+        // 10.9 vs 11.9 us).
+        if (dt == README_BF16 && 2 * wbytes <= 131072 && T <= 4096) {
+            switch (cpl) {
+                case 1: return launch_route_f32w<1>(T, d, E, x, w, bias, ids, logits, s);
+                case 2: return launch_route_f32w<2>(T, d, E, x, w, bias, ids, logits, s);
+                case 4: return launch_route_f32w<4>(T, d, E, x, w, bias, ids, logits, s);
+                case 8: return launch_route_f32w<8>(T, d, E, x, w, bias, ids, logits, s);
+                default: break;
+            }
+        }
         if (wbytes <= 65536) {
             if (dt == README_BF16)
                 return launch_route_lds<8, 65536>(cpl, T, d, E, x, w, bias, ids, logits, s);

@@ -48,7 +48,8 @@ def test_route_bit_exact(L, oracle_mod, name):
 
 @pytest.mark.parametrize("T,d,E,dtype", [(1, 8, 1, "bf16"), (5, 24, 3, "bf16"),
                                          (70, 4, 2, "f32"), (300, 520, 37, "bf16"),
-                                         (9000, 256, 16, "bf16"), (130, 1032, 256, "bf16")])
+                                         (9000, 256, 16, "bf16"), (130, 1032, 256, "bf16"),
+                                         (33, 4096, 4, "bf16"), (4096, 2048, 16, "bf16")])
 def test_route_odd_shapes_and_ties(L, oracle_mod, T, d, E, dtype):
     w = wl.Workload("t", T=T, d=d, E=E, I=8, dtype=dtype, bias="zipf1")
     _say("route shape", T, d, E, dtype)
