@@ -392,6 +392,18 @@ def algorithmic(w: wl.Workload, counts: np.ndarray, fused: bool = False) -> dict
     }
 
 
+def cpu_model() -> str:
+    """The host CPU's model name, as /proc/cpuinfo gives it."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w: wl.Workload, target_s: float) -> dict:
     """The oracle as it stands on this host: the full path (route, group,
     gather, fp64 expert FFN, ungroup) on the first S tokens, repeated until
@@ -426,7 +438,7 @@ def cpu_baseline(w: wl.Workload, target_s: float) -> dict:
         total += run(S)
         reps += 1
     return {"value": reps * S / total, "unit": "tokens/s", "cores": oracle.threads(),
-            "kind": "oracle",
+            "cpu": cpu_model(), "kind": "oracle",
             "sample": f"first {S} of {w.T} tokens of the {w.name} workload, full path "
                       f"(route, {'top-%d, ' % w.K if w.K > 1 else ''}group, gather, fp64 expert FFN"
                       f"{' + permanent expert' if w.P else ''}, "
@@ -507,7 +519,8 @@ def main():
     wall = time.perf_counter() - t0
     gpu_ms = start.elapsed_time(stop)
     ms_per_step = gpu_ms / K
-    dom_us = 1e3 * float(np.mean([a.elapsed_time(b) for a, b in ev_dom]))
+    dom_all = np.array([1e3 * a.elapsed_time(b) for a, b in ev_dom])
+    dom_us = float(dom_all.mean())
     # Per-call breakdown: a separate, shorter pass after the timed region.
     for i in range(min(K, 20)):
         step(W + K + i, "all")
@@ -559,6 +572,8 @@ def main():
                           + (f", top-{w.K} (token, slot) pairs" if w.K > 1 else "")
                           + (", rows gathered through perm)" if fused else ")"))
         roof["launch_us"] = round(dom_us, 2)
+        roof["launch_us_p10_p50_p90"] = [round(float(v), 2)
+                                         for v in np.percentile(dom_all, [10, 50, 90])]
         if dom == "gate_up" and fused and not args.gemm_tile:
             roof["traffic"] = traffic_bytes(w.name)
         roof["algorithmic_bytes"] = int(wk["bytes"])
@@ -591,6 +606,9 @@ def main():
         # event pair before each call, from a separate 20-step pass after the
         # timed region (events between every call add their own gaps)
         "kernels_us": {k: (round(v, 2) if v is not None else None) for k, v in kern_us.items()},
+        # algorithmic bytes of each call over its breakdown time (HBM peak 8000 GB/s)
+        "kernels_gbs": {k: round(work[k]["bytes"] / (v * 1e-6) / 1e9, 1)
+                        for k, v in kern_us.items() if v and k in work},
         "host_wall_ms_per_step": round(1e3 * wall / K, 4),
         "roofline": roof,
     }
