@@ -449,8 +449,9 @@ def cpu_baseline(w: wl.Workload, target_s: float) -> dict:
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the multi-GPU sharding is a design note, not a measured path.", file=sys.stderr)
+        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}); "
+              "sharding across GPUs is described in the design notes, not measured.",
+              file=sys.stderr)
         sys.exit(2)
     import torch
     if not torch.cuda.is_available():

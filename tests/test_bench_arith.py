@@ -61,3 +61,15 @@ def test_decode_stack_counts_active_experts_only():
     n, d, I = 64, 4096, 1376
     assert a["stack"]["bytes"] == 32 * (per_layer_weights + 3 * n * d * 4 + 2 * n * (d + I) * 2)
     assert a["stack"]["flops"] == 6.0 * n * d * I * 32
+
+
+def test_more_than_one_gpu_is_refused():
+    """bench.py measures one GPU; --gpus N > 1 exits with a message before
+    touching a device."""
+    import subprocess
+    import sys
+    from pathlib import Path
+    r = subprocess.run([sys.executable, str(Path(bench.__file__)), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
