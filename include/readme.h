@@ -450,13 +450,39 @@ readme_status readme_cache_simulate(int32_t policy, int64_t capacity, int64_t n,
  *   bit.  counts [E] (host) are the token counts of `offsets` (the caller's
  *   scheduler knows them: no device read), next_counts [E] (host, or NULL)
  *   those of the next step, which the Belady rule looks ahead to.  Needs
- *   slots >= 2 * (experts with tokens); else README_ERR_UNSUPPORTED.  A
- *   miss evicts, among slots not used by the layer being loaded or the layer
- *   before it, the key referenced farthest ahead (lowest key on ties) or the
- *   least recently referenced one.  Host side: plans the whole step, then
- *   enqueues; it waits on the host only for the copy of its slot table from
- *   two steps earlier.  Calls on one executor must not overlap.
+ *   slots >= 2 * (experts with tokens); else README_ERR_UNSUPPORTED.  The
+ *   step's placement is planned as readme_offload_plan states; a plan that
+ *   fails leaves the cache unchanged and nothing enqueued.  Host side: plans
+ *   the whole step, then enqueues; it waits on the host only for the copy
+ *   of its slot table from two steps earlier.  If an enqueue fails
+ *   (README_ERR_HIP) the executor forgets every cached key.  Calls on one
+ *   executor must not overlap.
  * readme_offload_stats -- cumulative hits, misses and bytes copied.
+ * readme_offload_last_plan -- the references of the last successful
+ *   readme_offload_stack step, in reference order (layer by layer, experts
+ *   ascending): hits [n] (1 = hit), slot [n] (the slot that layer reads the
+ *   expert from), evicted [n] (the key a miss evicted, layer*E+expert, -1
+ *   none); *n_refs = n.  README_ERR_WORKSPACE if n > max_refs (*n_refs is
+ *   still set).  Host only.
+ *
+ * readme_offload_plan -- the executor's placement planner alone (host only,
+ *   no GPU): a cache of `slots` (layer, expert) entries, key layer*E+expert,
+ *   over n_steps steps whose tokens per expert are counts [n_steps][E]
+ *   (host).  A step references, for l = 0 .. L-1, the key of every expert
+ *   with tokens, ascending.  A reference hits if its key is cached; a miss
+ *   takes the lowest empty slot, else evicts, among the slots this step has
+ *   NOT used at layer l or at layer l-1 (their kernels are enqueued after
+ *   the copy), by policy:
+ *     README_CACHE_BELADY  the key whose next reference is farthest ahead
+ *                          (never = farthest), lowest key on ties, looking
+ *                          at the rest of the step and, if lookahead != 0,
+ *                          at the next step's references (Sec. 4.1);
+ *     README_CACHE_LRU     the least recently referenced key.
+ *   Out, per reference in order: hits, slot, evicted as for
+ *   readme_offload_last_plan; *n_refs = references written.
+ *   README_ERR_UNSUPPORTED if a step has more than slots / 2 experts with
+ *   tokens, README_ERR_WORKSPACE if more than max_refs references,
+ *   README_ERR_ARG for a bad size, policy or count.
  * readme_offload_destroy -- waits for the executor's copies and for the last
  *   recorded layer of the compute stream, then frees everything.
  */
@@ -473,6 +499,15 @@ readme_status readme_offload_stack(readme_offload *ex, int64_t T,
                                    void *stream);
 readme_status readme_offload_stats(const readme_offload *ex, int64_t *hits,
                                    int64_t *misses, int64_t *bytes_copied);
+readme_status readme_offload_last_plan(const readme_offload *ex, int64_t max_refs,
+                                       uint8_t *hits, int32_t *slot,
+                                       int32_t *evicted, int64_t *n_refs);
+readme_status readme_offload_plan(int32_t E, int32_t L, int32_t slots,
+                                  int32_t policy, int32_t n_steps,
+                                  const int32_t *counts, int32_t lookahead,
+                                  int64_t max_refs, uint8_t *hits,
+                                  int32_t *slot, int32_t *evicted,
+                                  int64_t *n_refs);
 void readme_offload_destroy(readme_offload *ex);
 
 /*

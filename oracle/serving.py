@@ -122,3 +122,80 @@ def cache_simulate(refs, capacity: int, policy: str, seed: int = 0):
         last_use[key] = t
         evicted.append(victim)
     return hits, evicted
+
+
+def offload_plan(counts_per_step, E: int, L: int, slots: int, policy: str,
+                 lookahead: bool = True):
+    """Placement plan of the expert-offload executor (Sec. 4.1): a device
+    cache of `slots` (layer, expert) entries, key = layer * E + expert.
+
+    Step s references, for every layer l = 0 .. L-1 in order, the key of
+    every expert with tokens that step (ascending expert index).  A hit
+    reuses the key's slot.  A miss takes the lowest-numbered empty slot;
+    when none is empty it evicts, among the slots that step s has NOT used
+    at layer l or at layer l-1 (the executor copies layer l's experts
+    before layer l-1's kernels run, so those slots are still to be read):
+      belady  the key whose next reference is farthest ahead (never again
+              = farthest; lowest key on ties), the references being the
+              rest of step s and then, with lookahead, step s+1's;
+      lru     the least recently referenced key.
+    A step with more than slots / 2 experts with tokens cannot be placed
+    (two layers' experts must fit at once): ValueError.
+
+    Returns one (hit, slot, evicted key or -1) per reference, in order.
+    """
+    slot_key = [-1] * slots      # key held by each slot
+    slot_layer = [-1] * slots    # layer of the slot's last use
+    slot_step = [-1] * slots     # step of that use
+    last_ref = {}                # key -> time of its last reference (lru)
+    clock = 0
+    out = []
+    for s, counts in enumerate(counts_per_step):
+        active = [e for e in range(E) if counts[e] > 0]
+        if 2 * len(active) > slots:
+            raise ValueError("the cache cannot hold two layers' experts")
+        nxt = []
+        if lookahead and s + 1 < len(counts_per_step):
+            nxt = [e for e in range(E) if counts_per_step[s + 1][e] > 0]
+        refs = [l * E + e for l in range(L) for e in active]
+        refs += [l * E + e for l in range(L) for e in nxt]
+        pos = 0
+        for l in range(L):
+            for e in active:
+                key = l * E + e
+                clock += 1
+                if key in slot_key:
+                    q = slot_key.index(key)
+                    out.append((True, q, -1))
+                else:
+                    victim = -1
+                    empty = [q for q in range(slots) if slot_key[q] < 0]
+                    if empty:
+                        q = empty[0]
+                    else:
+                        best = None      # (value, key, slot); larger value = better victim
+                        for c in range(slots):
+                            if slot_step[c] == s and slot_layer[c] in (l, l - 1):
+                                continue
+                            k = slot_key[c]
+                            if policy == "belady":
+                                value = INF
+                                for u in range(pos + 1, len(refs)):
+                                    if refs[u] == k:
+                                        value = u
+                                        break
+                            elif policy == "lru":
+                                value = -last_ref[k]
+                            else:
+                                raise ValueError(f"unknown policy {policy}")
+                            if best is None or value > best[0] or (value == best[0] and k < best[1]):
+                                best = (value, k, c)
+                        q = best[2]
+                        victim = slot_key[q]
+                    slot_key[q] = key
+                    out.append((False, q, victim))
+                slot_layer[q] = l
+                slot_step[q] = s
+                last_ref[key] = clock
+                pos += 1
+    return out

@@ -68,6 +68,9 @@ SIGNATURES = {
     "readme_offload_stack": (_I32, [_P, _I64, _P, _P, _P, _P, _F, _P, _SZ, _P]),
     "readme_offload_stats": (_I32, [_P, _P, _P, _P]),
     "readme_offload_destroy": (None, [_P]),
+    "readme_offload_last_plan": (_I32, [_P, _I64, _P, _P, _P, _P]),
+    "readme_offload_plan": (_I32, [_I32, _I32, _I32, _I32, _I32, _P, _I32, _I64, _P, _P, _P,
+                                   _P]),
     "readme_ungroup": (_I32, [_I32, _I64, _I64, _P, _P, _P, _P]),
     "readme_moe_ffn_stack_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
     "readme_moe_ffn_stack": (_I32, [_I64, _I64, _I32, _I64, _I32, _P, _P, _P, _F, _P,
@@ -459,6 +462,25 @@ def readme_cache_simulate(refs, capacity: int, policy: str, seed: int = 0):
     return hits[:n].astype(bool).tolist(), evicted[:n].tolist(), nh.value
 
 
+def readme_offload_plan(counts_per_step, E: int, L: int, slots: int, policy: str,
+                        lookahead: bool = True):
+    """The offload executor's placement planner on host counts [steps][E];
+    returns one (hit, slot, evicted key or -1) per reference."""
+    import numpy as np
+    counts, p_counts = _host_i32(np.asarray(counts_per_step, np.int64).reshape(-1, E))
+    n_steps = counts.shape[0]
+    cap = max(1, int(L * (counts > 0).sum()))
+    hits = np.zeros(cap, np.uint8)
+    slot = np.zeros(cap, np.int32)
+    evicted = np.zeros(cap, np.int32)
+    n = ctypes.c_int64(0)
+    _call("readme_offload_plan", E, L, slots, README_CACHE_POLICIES[policy], n_steps, p_counts,
+          1 if lookahead else 0, cap, hits.ctypes.data_as(ctypes.c_void_p),
+          slot.ctypes.data_as(ctypes.c_void_p), evicted.ctypes.data_as(ctypes.c_void_p),
+          ctypes.byref(n))
+    return [(bool(hits[i]), int(slot[i]), int(evicted[i])) for i in range(n.value)]
+
+
 class Offload:
     """Expert-offload executor (readme_offload_*): packed layers in pinned host
     memory, `slots` device slots, copies one layer ahead on its own stream."""
@@ -486,6 +508,22 @@ class Offload:
               rms_eps, _p(workspace), workspace.numel() * workspace.element_size(),
               _stream(x_resid_grouped.device))
         return x_resid_grouped
+
+    def last_plan(self):
+        """The last step's references: (hit, slot, evicted key or -1) each."""
+        import numpy as np
+        n = ctypes.c_int64(0)
+        st = load().readme_offload_last_plan(self.h, 0, None, None, None, ctypes.byref(n))
+        if st not in (0, 3):
+            raise ReadmeError("readme_offload_last_plan", st)
+        cap = max(1, n.value)
+        hits = np.zeros(cap, np.uint8)
+        slot = np.zeros(cap, np.int32)
+        evicted = np.zeros(cap, np.int32)
+        _call("readme_offload_last_plan", self.h, cap, hits.ctypes.data_as(ctypes.c_void_p),
+              slot.ctypes.data_as(ctypes.c_void_p), evicted.ctypes.data_as(ctypes.c_void_p),
+              ctypes.byref(n))
+        return [(bool(hits[i]), int(slot[i]), int(evicted[i])) for i in range(n.value)]
 
     def stats(self):
         h, m, b = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()

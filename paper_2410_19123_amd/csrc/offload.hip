@@ -8,19 +8,18 @@
 // Ordering.  Per layer l the copy stream records ready[l] after its copies
 // and the compute stream waits on it; the compute stream records done[l]
 // after the layer's down projection, and before a copy overwrites a slot
-// the copy stream waits on done[] of the slot's last layer.  Keys of the
-// layer about to be computed and of the one being loaded are never evicted,
-// so a slot is never overwritten while a kernel enqueued before the copy
-// may still read it.
+// the copy stream waits on done[] of the slot's last layer.  The planner
+// (offload_plan.cpp) never overwrites a slot this step used at the layer
+// being loaded or at the one before it, whose kernels are enqueued after
+// the copy, so a slot is never overwritten while a kernel may still read it.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <limits>
-#include <unordered_map>
 #include <vector>
 
 #include "common.hpp"
 #include "internal.hpp"
+#include "offload_plan.hpp"
 
 using namespace readme;
 
@@ -36,13 +35,8 @@ struct readme_offload {
     std::vector<hipEvent_t> ready, done;
     hipEvent_t table_done[2] = {nullptr, nullptr};
     bool table_used[2] = {false, false};
-    std::vector<int32_t> slot_key;   // key l*E+e held by a slot, -1 empty
-    std::vector<int32_t> slot_layer; // layer of the slot's last compute use, -1 none
-    std::vector<int64_t> slot_step;  // step of that use
-    std::unordered_map<int32_t, int32_t> where;  // key -> slot
-    std::unordered_map<int32_t, int64_t> last_ref;  // LRU: key -> reference time
-    int64_t clock = 0;
-    int64_t step = 0;
+    OffloadCache cache;              // which (layer, expert) each slot holds
+    std::vector<OffloadRef> last_plan;  // the references of the last step
     int64_t hits = 0, misses = 0, bytes = 0;
 };
 
@@ -126,9 +120,7 @@ readme_status readme_offload_create(int32_t E, int64_t d, int64_t I, int32_t L, 
         release(ex);
         return README_ERR_HIP;
     }
-    ex->slot_key.assign(slots, -1);
-    ex->slot_layer.assign(slots, -1);
-    ex->slot_step.assign(slots, -1);
+    ex->cache.init(E, L, slots, policy);
     *out = ex;
     return README_OK;
 }
@@ -156,95 +148,35 @@ readme_status readme_offload_stack(readme_offload* ex, int64_t T, const int32_t*
     const int E = ex->E, L = ex->L;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
 
-    // References of this step in layer order (then the next step's, for the
-    // Belady look-ahead).
-    std::vector<int32_t> active, next_active;
-    for (int e = 0; e < E; ++e) {
-        if (counts[e] < 0) return README_ERR_ARG;
-        if (counts[e] > 0) active.push_back(e);
-        if (next_counts && next_counts[e] > 0) next_active.push_back(e);
-    }
-    // Two layers' experts (the one being loaded and the one computed before
-    // it) must fit in the cache at once.
-    const int A = (int)active.size();
-    if (2 * A > ex->slots) return README_ERR_UNSUPPORTED;
-    std::vector<int32_t> refs;
-    for (int l = 0; l < L; ++l)
-        for (int e : active) refs.push_back(l * E + e);
-    for (int l = 0; l < L; ++l)
-        for (int e : next_active) refs.push_back(l * E + e);
-    const int64_t NEVER = std::numeric_limits<int64_t>::max();
-    std::unordered_map<int32_t, std::vector<int64_t>> uses;  // key -> positions, ascending
-    for (int64_t t = 0; t < (int64_t)refs.size(); ++t) uses[refs[t]].push_back(t);
-    auto next_use = [&](int32_t key, int64_t after) {
-        auto it = uses.find(key);
-        if (it == uses.end()) return NEVER;
-        auto p = std::upper_bound(it->second.begin(), it->second.end(), after);
-        return p == it->second.end() ? NEVER : *p;
-    };
+    for (int e = 0; e < E; ++e)
+        if (counts[e] < 0 || (next_counts && next_counts[e] < 0)) return README_ERR_ARG;
 
     // The slot table buffer of this step's parity was last copied two steps
     // ago; make sure that copy finished before the host rewrites it.
-    const int par = (int)(ex->step & 1);
+    const int par = (int)(ex->cache.step & 1);
     if (ex->table_used[par] && hipEventSynchronize(ex->table_done[par]) != hipSuccess)
         return README_ERR_HIP;
+
+    // Plan every layer's placement first (it depends only on the references);
+    // the planner leaves the cache state unchanged if it fails.
+    std::vector<OffloadRef> plan;
+    const readme_status pst = offload_plan_step(ex->cache, counts, next_counts, plan);
+    if (pst != README_OK) return pst;
     int32_t* table = ex->host_index + (size_t)par * L * E;
     std::fill(table, table + (size_t)L * E, 0);
-
-    // Plan every layer's placement first (it depends only on the references).
     struct Copy { int32_t slot, layer, e, wait_layer; };
     std::vector<std::vector<Copy>> copies(L);
-    int64_t pos = 0;
-    for (int l = 0; l < L; ++l) {
-        for (int e : active) {
-            const int32_t key = l * E + e;
-            ++ex->clock;
-            auto it = ex->where.find(key);
-            int32_t slot;
-            if (it != ex->where.end()) {
-                slot = it->second;
-                ++ex->hits;
-            } else {
-                ++ex->misses;
-                slot = -1;
-                for (int32_t q = 0; q < ex->slots && slot < 0; ++q)
-                    if (ex->slot_key[q] < 0) slot = q;
-                if (slot < 0) {
-                    // Victim among keys not of layer l (being placed) nor
-                    // used at layer l-1 of this step (its compute is
-                    // enqueued after these copies).
-                    int64_t best = -1;
-                    int32_t best_key = 0;
-                    for (int32_t q = 0; q < ex->slots; ++q) {
-                        const int32_t k = ex->slot_key[q];
-                        const bool now = ex->slot_step[q] == ex->step;
-                        if (k / E == l || (now && ex->slot_layer[q] == l - 1)) continue;
-                        int64_t v;
-                        if (ex->policy == README_CACHE_BELADY)
-                            v = next_use(k, pos);                     // farthest next use
-                        else
-                            v = NEVER - ex->last_ref[k];              // least recent
-                        if (v > best || (v == best && k < best_key)) {
-                            best = v;
-                            best_key = k;
-                            slot = q;
-                        }
-                    }
-                    if (slot < 0) return README_ERR_UNSUPPORTED;  // cache too small
-                    ex->where.erase(ex->slot_key[slot]);
-                }
-                copies[l].push_back({slot, l, e, ex->slot_layer[slot]});
-                ex->slot_key[slot] = key;
-                ex->where[key] = slot;
-                ex->bytes += (int64_t)ex->slot_bytes;
-            }
-            ex->slot_layer[slot] = l;
-            ex->slot_step[slot] = ex->step;
-            ex->last_ref[key] = ex->clock;
-            table[(size_t)l * E + e] = slot;
-            ++pos;
+    for (const OffloadRef& r : plan) {
+        table[(size_t)r.layer * E + r.expert] = r.slot;
+        if (r.hit) {
+            ++ex->hits;
+        } else {
+            ++ex->misses;
+            ex->bytes += (int64_t)ex->slot_bytes;
+            copies[r.layer].push_back({r.slot, r.layer, r.expert, r.wait_layer});
         }
     }
+    ex->last_plan = plan;
 
     auto issue = [&](int l) -> bool {
         for (const Copy& c : copies[l]) {
@@ -263,6 +195,13 @@ readme_status readme_offload_stack(readme_offload* ex, int64_t T, const int32_t*
         return hipEventRecord(ex->ready[l], ex->copy) == hipSuccess;
     };
 
+    // A failure past this point leaves copies unissued for keys the plan
+    // already counts as cached: forget every key, so no later step hits on a
+    // slot whose copy never ran.
+    auto fail = [&]() {
+        ex->cache.clear();
+        return README_ERR_HIP;
+    };
     int32_t* dev_table = ex->dev_index + (size_t)par * L * E;
     // The copy stream starts after the work already on the compute stream.
     hipEvent_t start = ex->done[L - 1];
@@ -270,9 +209,9 @@ readme_status readme_offload_stack(readme_offload* ex, int64_t T, const int32_t*
         hipMemcpyAsync(dev_table, table, sizeof(int32_t) * L * E, hipMemcpyHostToDevice,
                        ex->copy) != hipSuccess ||
         hipEventRecord(ex->table_done[par], ex->copy) != hipSuccess)
-        return README_ERR_HIP;
+        return fail();
     ex->table_used[par] = true;
-    if (!issue(0)) return README_ERR_HIP;
+    if (!issue(0)) return fail();
 
     uint16_t* xn = reinterpret_cast<uint16_t*>(workspace);
     uint16_t* h = xn + T * ex->d;
@@ -280,8 +219,8 @@ readme_status readme_offload_stack(readme_offload* ex, int64_t T, const int32_t*
     for (int e = 0; e < E; ++e) m32 += (counts[e] + 31) / 32;
     const int64_t slot_elems = (int64_t)(ex->slot_bytes / 2);
     for (int l = 0; l < L; ++l) {
-        if (l + 1 < L && !issue(l + 1)) return README_ERR_HIP;
-        if (hipStreamWaitEvent(s, ex->ready[l], 0) != hipSuccess) return README_ERR_HIP;
+        if (l + 1 < L && !issue(l + 1)) return fail();
+        if (hipStreamWaitEvent(s, ex->ready[l], 0) != hipSuccess) return fail();
         hipError_t err = launch_rms_to_bf16(T, ex->d, x_resid_grouped, offsets, E, rms_eps, xn, s);
         GemmArgs gu = gate_up_args(README_BF16, T, ex->d, E, ex->I, xn, offsets, ex->dev_slots, h);
         gu.b_expert_stride = slot_elems;
@@ -295,10 +234,25 @@ readme_status readme_offload_stack(readme_offload* ex, int64_t T, const int32_t*
         dn.b_index = dev_table + (size_t)l * E;
         dn.m_tiles32 = m32;
         if (err == hipSuccess) err = launch_grouped_gemm(false, EPI_RESID_ADD, dn, s);
-        if (err != hipSuccess || hipEventRecord(ex->done[l], s) != hipSuccess)
-            return README_ERR_HIP;
+        if (err != hipSuccess || hipEventRecord(ex->done[l], s) != hipSuccess) return fail();
     }
-    ++ex->step;
+    return README_OK;
+}
+
+readme_status readme_offload_last_plan(const readme_offload* ex, int64_t max_refs,
+                                       uint8_t* hits, int32_t* slot, int32_t* evicted,
+                                       int64_t* n_refs) {
+    if (!ex || max_refs < 0 || !n_refs) return README_ERR_ARG;
+    const int64_t n = (int64_t)ex->last_plan.size();
+    *n_refs = n;
+    if (n > max_refs) return README_ERR_WORKSPACE;
+    if (n > 0 && (!hits || !slot || !evicted)) return README_ERR_ARG;
+    for (int64_t i = 0; i < n; ++i) {
+        const OffloadRef& r = ex->last_plan[i];
+        hits[i] = r.hit ? 1 : 0;
+        slot[i] = r.slot;
+        evicted[i] = r.evicted;
+    }
     return README_OK;
 }
 

@@ -153,3 +153,180 @@ def test_native_argument_errors(lib):
                                  ctypes.byref(nv)) == 1
     assert L.readme_expert_batch(0, offs, items, 4, out, ctypes.byref(bl), out, out,
                                  ctypes.byref(nv)) == 1
+
+
+# ------------------------------------------------- offload placement (Sec. 4.1)
+def _golden_offload():
+    for line in open(os.path.join(GOLD, "offload_plan.txt")):
+        if not line.strip() or line.startswith("#"):
+            continue
+        E, L, slots, policy, steps, plan = [f.strip() for f in line.split(";")]
+        E, L = int(E), int(L)
+        counts = []
+        for st in steps.split("|"):
+            c = [0] * E
+            for e in _ints(st):
+                c[e] = 1
+            counts.append(c)
+        want = []
+        for tok in plan.split():
+            if tok[0] == "h":
+                want.append((True, int(tok[1:]), -1))
+            else:
+                slot, _, ev = tok[1:].partition("-1") if tok.endswith("-1") else (None, None, None)
+                if slot is not None and ":" not in tok:
+                    want.append((False, int(slot), -1))
+                else:
+                    s, ev = tok[1:].split(":")
+                    want.append((False, int(s), int(ev)))
+        yield E, L, int(slots), policy, counts, want
+
+
+def test_offload_plan_hand_derived():
+    cases = list(_golden_offload())
+    assert len(cases) == 3
+    for E, L, slots, policy, counts, want in cases:
+        assert S.offload_plan(counts, E, L, slots, policy) == want, (E, L, slots, policy)
+
+
+def _random_steps(rng, E, n_steps, max_active):
+    out = []
+    for _ in range(n_steps):
+        k = int(rng.integers(1, max_active + 1))
+        c = [0] * E
+        for e in rng.choice(E, size=k, replace=False):
+            c[int(e)] = int(rng.integers(1, 5))
+        out.append(c)
+    return out
+
+
+def _min_misses(counts, E, L, slots):
+    """Fewest misses any victim choice reaches over the steps, under the same
+    protection rule (exhaustive search with memoisation)."""
+    refs = []
+    for s, c in enumerate(counts):
+        for l in range(L):
+            for e in range(E):
+                if c[e] > 0:
+                    refs.append((s, l, l * E + e))
+
+    @functools.lru_cache(maxsize=None)
+    def go(i, keys, layers, steps):
+        if i == len(refs):
+            return 0
+        s, l, key = refs[i]
+        keys, layers, steps = list(keys), list(layers), list(steps)
+        if key in keys:
+            q = keys.index(key)
+            layers[q], steps[q] = l, s
+            return go(i + 1, tuple(keys), tuple(layers), tuple(steps))
+        if -1 in keys:
+            choices = [keys.index(-1)]
+        else:
+            choices = [q for q in range(slots) if not (steps[q] == s and layers[q] in (l, l - 1))]
+        best = None
+        for q in choices:
+            k2, l2, s2 = keys[:], layers[:], steps[:]
+            k2[q], l2[q], s2[q] = key, l, s
+            v = go(i + 1, tuple(k2), tuple(l2), tuple(s2))
+            best = v if best is None or v < best else best
+        return 1 + best
+
+    return go(0, (-1,) * slots, (-1,) * slots, (-1,) * slots)
+
+
+def test_offload_plan_belady_is_optimal_on_tiny_traces():
+    """Over one or two steps the look-ahead (the next step) covers every
+    future reference, and the Belady choice among unprotected slots then
+    reaches the fewest misses over every victim choice the protection rule
+    allows (checked exhaustively on tiny traces; LRU does not, which shows
+    the check can fail).  With more steps the executor sees one step ahead
+    only, so it is not optimal over the whole trace."""
+    rng = np.random.default_rng(7)
+    lru_worse = 0
+    for _ in range(300):
+        E, L = int(rng.integers(2, 5)), int(rng.integers(2, 4))
+        n_steps = int(rng.integers(1, 3))
+        counts = _random_steps(rng, E, n_steps, min(2, E))
+        A = max(sum(1 for v in c if v > 0) for c in counts)
+        slots = int(rng.integers(2 * A, 2 * A + 3))
+        best = _min_misses(counts, E, L, slots)
+        plan = S.offload_plan(counts, E, L, slots, "belady")
+        assert sum(1 for h, _, _ in plan if not h) == best, (counts, E, L, slots)
+        lru = S.offload_plan(counts, E, L, slots, "lru")
+        lru_worse += sum(1 for h, _, _ in lru if not h) > best
+    assert lru_worse > 0
+
+
+def test_offload_plan_lru_is_textbook_lru():
+    """The protected slots are the most recently used ones, so the LRU plan
+    is plain LRU over the flattened references (cache_simulate)."""
+    rng = np.random.default_rng(8)
+    for _ in range(100):
+        E, L = int(rng.integers(2, 7)), int(rng.integers(1, 5))
+        counts = _random_steps(rng, E, int(rng.integers(1, 6)), min(3, E))
+        A = max(sum(1 for v in c if v > 0) for c in counts)
+        slots = int(rng.integers(2 * A, 2 * A + 5))
+        refs = [l * E + e for c in counts for l in range(L) for e in range(E) if c[e] > 0]
+        hits, evicted = S.cache_simulate(refs, slots, "lru")
+        plan = S.offload_plan(counts, E, L, slots, "lru")
+        assert [h for h, _, _ in plan] == hits
+        assert [v for _, _, v in plan] == evicted
+
+
+def test_offload_plan_invariants():
+    rng = np.random.default_rng(9)
+    for policy in ("belady", "lru"):
+        for _ in range(60):
+            E, L = int(rng.integers(2, 9)), int(rng.integers(1, 6))
+            counts = _random_steps(rng, E, int(rng.integers(1, 8)), min(4, E))
+            A = max(sum(1 for v in c if v > 0) for c in counts)
+            slots = int(rng.integers(2 * A, 2 * A + 6))
+            plan = S.offload_plan(counts, E, L, slots, policy)
+            held = [-1] * slots
+            i = 0
+            for c in counts:
+                for l in range(L):
+                    for e in range(E):
+                        if c[e] == 0:
+                            continue
+                        hit, q, ev = plan[i]
+                        i += 1
+                        assert 0 <= q < slots
+                        if hit:
+                            assert held[q] == l * E + e and ev == -1
+                        else:
+                            assert held[q] == ev     # evicts what the slot held
+                            held[q] = l * E + e
+            assert i == len(plan)
+
+
+def test_offload_plan_refuses_small_cache():
+    with pytest.raises(ValueError):
+        S.offload_plan([[1, 1, 1, 0]], 4, 2, 5, "belady")
+
+
+def test_native_offload_plan_equals_oracle(lib):
+    native = lib
+    rng = np.random.default_rng(10)
+    for policy in ("belady", "lru"):
+        for look in (True, False):
+            for _ in range(80):
+                E, L = int(rng.integers(1, 17)), int(rng.integers(1, 9))
+                counts = _random_steps(rng, E, int(rng.integers(1, 10)), min(5, E))
+                A = max(sum(1 for v in c if v > 0) for c in counts)
+                slots = int(rng.integers(2 * A, 2 * A + 9))
+                assert (native.readme_offload_plan(counts, E, L, slots, policy, look)
+                        == S.offload_plan(counts, E, L, slots, policy, look))
+    for E, L, slots, policy, counts, want in _golden_offload():
+        assert native.readme_offload_plan(counts, E, L, slots, policy) == want
+
+
+def test_native_offload_plan_errors(lib):
+    native = lib
+    with pytest.raises(native.ReadmeError) as e:
+        native.readme_offload_plan([[1, 1, 1, 0]], 4, 2, 5, "belady")
+    assert e.value.status == 2
+    with pytest.raises(native.ReadmeError) as e:
+        native.readme_offload_plan([[1, -1]], 2, 2, 4, "lru")
+    assert e.value.status == 1
