@@ -26,7 +26,9 @@
  *
  * Conventions for every call:
  *   - Arrays are DEVICE pointers owned by the caller, row-major, contiguous.
- *     The library keeps no state and owns no memory between calls.
+ *     The library owns no memory between calls and keeps no state, apart
+ *     from the executor objects a caller creates (readme_offload_*) and the
+ *     calling thread's tile override (readme_set_gemm_tile).
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     Calls only enqueue work on it: they never synchronise, allocate or
  *     free, and they read no device data on the host, so a caller may
@@ -155,8 +157,9 @@ readme_status readme_pack_experts(readme_dtype dt, int32_t E, int64_t d,
 int64_t readme_padded_intermediate(int64_t I);
 
 /*
- * readme_set_gemm_tile -- choose the workgroup tile of the grouped GEMMs,
- * process-wide, for tuning and for testing every configuration.
+ * readme_set_gemm_tile -- force one workgroup tile for the grouped GEMMs that
+ * the CALLING HOST THREAD launches (thread-local: other threads keep their
+ * own setting, 0 at start), for tuning and for testing every configuration.
  *   0 = automatic (by tokens per expert, the default)
  *   both operands staged in LDS:
  *     1 = 256x256, 2 = 256x128, 3 = 128x128, 4 = 128x256, 5 = 64x128,
@@ -169,10 +172,11 @@ int64_t readme_padded_intermediate(int64_t I);
  *     21 = 192x256 (3 stages), 22 = 192x256 (2 stages), 23 = 32x64
  *   (rows of tokens x columns of outputs)
  * Results do not depend on the tile beyond fp32 summation order.  Returns
- * README_ERR_ARG for any other value.  Not synchronised with calls in
- * flight on other host threads.
+ * README_ERR_ARG for any other value.  readme_get_gemm_tile returns the
+ * calling thread's current setting.
  */
 readme_status readme_set_gemm_tile(int32_t tile);
+int32_t readme_get_gemm_tile(void);
 
 /*
  * readme_moe_ffn -- each expert's SwiGLU FFN on its token block (Eq. 2 with
@@ -188,7 +192,13 @@ readme_status readme_set_gemm_tile(int32_t tile);
  *   y_grouped [T][d] dt out,
  *   workspace >= readme_moe_ffn_workspace_bytes(dt, T, I) bytes (holds h).
  * Requires d > 0 a multiple of 64, 1 <= E <= README_MAX_EXPERTS, I >= 1.
- * Offsets are read on the device only; a block range past T is clipped.
+ * Offsets are read on the device only, so the host cannot validate them:
+ * they must be readme_group_by_expert's (non-decreasing, within [0, T];
+ * offsets[E] < T when some ids were outside [0, E)).  The kernels clamp
+ * every block to [0, T], so a corrupt array cannot move an access outside
+ * the buffers, but the outputs are then unspecified; no flag reports it.
+ * Every streamed buffer (x_grouped, packed, y_grouped, workspace) must be
+ * 16-byte aligned, and all are checked before the first launch.
  */
 size_t readme_moe_ffn_workspace_bytes(readme_dtype dt, int64_t T, int64_t I);
 readme_status readme_moe_ffn(readme_dtype dt, int64_t T, int64_t d,

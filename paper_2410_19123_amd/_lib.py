@@ -36,6 +36,7 @@ SIGNATURES = {
     "readme_pack_experts": (_I32, [_I32, _I32, _I64, _I64, _P, _P, _P, _P, _SZ, _P]),
     "readme_padded_intermediate": (_I64, [_I64]),
     "readme_set_gemm_tile": (_I32, [_I32]),
+    "readme_get_gemm_tile": (_I32, []),
     "readme_moe_ffn_workspace_bytes": (_SZ, [_I32, _I64, _I64]),
     "readme_moe_ffn": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _SZ, _P]),
     "readme_moe_gate_up": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P]),

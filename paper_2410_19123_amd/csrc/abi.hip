@@ -131,6 +131,8 @@ readme_status readme_set_gemm_tile(int32_t tile) {
     return set_gemm_tile(tile) ? README_OK : README_ERR_ARG;
 }
 
+int32_t readme_get_gemm_tile(void) { return get_gemm_tile(); }
+
 readme_status readme_route(readme_dtype dt, int64_t T, int64_t d, int32_t E, const void* x,
                            const void* w_router, const float* bias, int32_t* expert_ids,
                            float* logits, void* stream) {
@@ -193,7 +195,7 @@ readme_status readme_moe_gate_up(readme_dtype dt, int64_t T, int64_t d, int32_t 
     if (st != README_OK) return st;
     if (T == 0) return README_OK;
     if (!x_grouped || !offsets || !packed || !h) return README_ERR_ARG;
-    if (!a16(x_grouped) || !a16(packed)) return README_ERR_ARG;
+    if (!a16(x_grouped) || !a16(packed) || !a16(h)) return README_ERR_ARG;
     GemmArgs g = gate_up_args(dt, T, d, E, I, x_grouped, offsets, packed, h);
     return hip_status(
         launch_grouped_gemm(dt == README_F32, EPI_GATE_UP_SILU, g, as_stream(stream)));
@@ -206,7 +208,7 @@ readme_status readme_moe_down(readme_dtype dt, int64_t T, int64_t d, int32_t E, 
     if (st != README_OK) return st;
     if (T == 0) return README_OK;
     if (!h || !offsets || !packed || !y_grouped) return README_ERR_ARG;
-    if (!a16(h) || !a16(packed)) return README_ERR_ARG;
+    if (!a16(h) || !a16(packed) || !a16(y_grouped)) return README_ERR_ARG;
     GemmArgs g = down_args(dt, T, d, E, I, h, offsets, packed, y_grouped);
     return hip_status(launch_grouped_gemm(dt == README_F32, EPI_STORE, g, as_stream(stream)));
 }
@@ -219,6 +221,10 @@ readme_status readme_moe_ffn(readme_dtype dt, int64_t T, int64_t d, int32_t E, i
     if (st != README_OK) return st;
     if (T == 0) return README_OK;
     if (!x_grouped || !offsets || !packed || !y_grouped || !workspace) return README_ERR_ARG;
+    // Every streamed buffer is checked before the first launch, so an error
+    // return means nothing was enqueued.
+    if (!a16(x_grouped) || !a16(packed) || !a16(y_grouped) || !a16(workspace))
+        return README_ERR_ARG;
     if (workspace_bytes < readme_moe_ffn_workspace_bytes(dt, T, I)) return README_ERR_WORKSPACE;
     st = readme_moe_gate_up(dt, T, d, E, I, x_grouped, offsets, packed, workspace, stream);
     if (st != README_OK) return st;
@@ -233,7 +239,7 @@ readme_status readme_moe_gate_up_gather(readme_dtype dt, int64_t T, int64_t d, i
     if (st != README_OK) return st;
     if (T == 0) return README_OK;
     if (!x || !perm || !offsets || !packed || !h) return README_ERR_ARG;
-    if (!a16(x) || !a16(packed)) return README_ERR_ARG;
+    if (!a16(x) || !a16(packed) || !a16(h)) return README_ERR_ARG;
     GemmArgs g = gate_up_args(dt, T, d, E, I, x, offsets, packed, h);
     g.a_rows = perm;  // grouped row j reads token row perm[j]
     return hip_status(
@@ -248,7 +254,7 @@ readme_status readme_moe_down_scatter(readme_dtype dt, int64_t T, int64_t d, int
     if (st != README_OK) return st;
     if (T == 0) return README_OK;
     if (!h || !perm || !offsets || !packed || !y) return README_ERR_ARG;
-    if (!a16(h) || !a16(packed)) return README_ERR_ARG;
+    if (!a16(h) || !a16(packed) || !a16(y)) return README_ERR_ARG;
     GemmArgs g = down_args(dt, T, d, E, I, h, offsets, packed, y);
     g.c_rows = perm;  // grouped row j lands in token row perm[j]
     return hip_status(launch_grouped_gemm(dt == README_F32, EPI_STORE, g, as_stream(stream)));
@@ -262,7 +268,7 @@ readme_status readme_moe_ffn_fused(readme_dtype dt, int64_t T, int64_t d, int32_
     if (st != README_OK) return st;
     if (T == 0) return README_OK;
     if (!x || !perm || !offsets || !packed || !y || !workspace) return README_ERR_ARG;
-    if (!a16(y) || !a16(workspace)) return README_ERR_ARG;
+    if (!a16(x) || !a16(packed) || !a16(y) || !a16(workspace)) return README_ERR_ARG;
     if (workspace_bytes < readme_moe_ffn_workspace_bytes(dt, T, I)) return README_ERR_WORKSPACE;
     st = readme_moe_gate_up_gather(dt, T, d, E, I, x, perm, offsets, packed, workspace, stream);
     if (st != README_OK) return st;
@@ -404,7 +410,7 @@ readme_status readme_moe_ffn_topk(readme_dtype dt, int64_t T, int64_t d, int32_t
     if (st != README_OK) return st;
     if (T == 0) return README_OK;
     if (!x || !perm || !offsets || !packed || !y_pairs || !workspace) return README_ERR_ARG;
-    if (!a16(y_pairs) || !a16(workspace)) return README_ERR_ARG;
+    if (!a16(x) || !a16(packed) || !a16(y_pairs) || !a16(workspace)) return README_ERR_ARG;
     if (workspace_bytes < readme_moe_ffn_workspace_bytes(dt, T * K, I)) return README_ERR_WORKSPACE;
     st = readme_moe_gate_up_gather_topk(dt, T, d, E, I, K, x, perm, offsets, packed, workspace,
                                         stream);

@@ -6,14 +6,18 @@
 
 namespace readme {
 
-static int g_forced_tile = TILE_AUTO;
-static int forced_tile() { return __atomic_load_n(&g_forced_tile, __ATOMIC_RELAXED); }
+// Tile override of the calling host thread (0 = automatic): a tuning and
+// test knob that affects only launches made from the thread that set it.
+static thread_local int t_forced_tile = TILE_AUTO;
+static int forced_tile() { return t_forced_tile; }
 
 bool set_gemm_tile(int tile) {
     if (tile < TILE_AUTO || tile > TILE_LAST) return false;
-    __atomic_store_n(&g_forced_tile, tile, __ATOMIC_RELAXED);
+    t_forced_tile = tile;
     return true;
 }
+
+int get_gemm_tile() { return t_forced_tile; }
 
 // Tile shape by tokens per expert (the host knows T and E, not the split):
 // many rows per expert favour large tiles (fewer LDS and L2 bytes per

@@ -73,6 +73,7 @@ GemmArgs gate_up_args(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t 
 GemmArgs down_args(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I, const void* h,
                    const int32_t* offsets, const void* packed, void* y);
 bool set_gemm_tile(int tile);
+int get_gemm_tile();
 hipError_t launch_topk(int64_t T, int E, int K, const float* logits, int32_t* ids, float* weights,
                        hipStream_t s);
 hipError_t launch_combine(bool f32, int64_t T, int64_t d, int K, const void* y_pairs,

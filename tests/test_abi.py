@@ -156,3 +156,43 @@ def test_stack_counts_argument_errors(lib):
     neg = (ctypes.c_int32 * 8)(1, 2, -1, 0, 0, 0, 0, 0)
     assert s(64, 4096, 8, 1376, 1, arr, FAKE, neg, FAKE, ctypes.c_float(1e-5), FAKE, 1 << 40,
              None) == 1                                          # negative count
+
+
+def test_streamed_buffers_checked_before_any_launch(lib):
+    """Every streamed buffer's alignment is checked on the host before the
+    first launch (no GPU here: a launch would report README_ERR_HIP)."""
+    big = 1 << 40
+    odd = ctypes.c_void_p(4104)     # 8-byte aligned only
+    f = lib.readme_moe_ffn
+    assert f(1, 16, 4096, 8, 1376, FAKE, FAKE, FAKE, FAKE, odd, big, None) == 1   # workspace
+    assert f(1, 16, 4096, 8, 1376, FAKE, FAKE, FAKE, odd, FAKE, big, None) == 1   # y_grouped
+    assert f(1, 16, 4096, 8, 1376, odd, FAKE, FAKE, FAKE, FAKE, big, None) == 1   # x_grouped
+    assert f(1, 16, 4096, 8, 1376, FAKE, FAKE, odd, FAKE, FAKE, big, None) == 1   # packed
+    gu = lib.readme_moe_gate_up
+    assert gu(1, 16, 4096, 8, 1376, FAKE, FAKE, FAKE, odd, None) == 1              # h
+    dn = lib.readme_moe_down
+    assert dn(1, 16, 4096, 8, 1376, FAKE, FAKE, FAKE, odd, None) == 1              # y_grouped
+    fu = lib.readme_moe_ffn_fused
+    assert fu(1, 16, 4096, 8, 1376, odd, FAKE, FAKE, FAKE, FAKE, FAKE, big, None) == 1  # x
+    assert fu(1, 16, 4096, 8, 1376, FAKE, FAKE, FAKE, FAKE, FAKE, odd, big, None) == 1  # workspace
+    g = lib.readme_moe_gate_up_gather
+    assert g(1, 16, 4096, 8, 1376, FAKE, FAKE, FAKE, FAKE, odd, None) == 1          # h
+    sc = lib.readme_moe_down_scatter
+    assert sc(1, 16, 4096, 8, 1376, FAKE, FAKE, FAKE, FAKE, odd, None) == 1         # y
+    t = lib.readme_moe_ffn_topk
+    assert t(1, 16, 4096, 8, 1376, 2, odd, FAKE, FAKE, FAKE, FAKE, FAKE, big, None) == 1
+
+
+def test_tile_override_is_per_thread(lib):
+    import threading
+    assert lib.readme_set_gemm_tile(24) == 1
+    assert lib.readme_set_gemm_tile(-1) == 1
+    assert lib.readme_set_gemm_tile(5) == 0
+    seen = []
+    th = threading.Thread(target=lambda: seen.append(lib.readme_get_gemm_tile()))
+    th.start()
+    th.join()
+    assert seen == [0]                       # another thread keeps the automatic choice
+    assert lib.readme_get_gemm_tile() == 5
+    assert lib.readme_set_gemm_tile(0) == 0
+    assert lib.readme_get_gemm_tile() == 0
