@@ -5,16 +5,20 @@ route (top-1 router) -> group (histogram, scan, stable permute, row gather)
 -> expert FFN (fused gate/up + SiLU*mul, then down) -> ungroup.  For the
 stacked decode workload a step is route + group + L layers + ungroup.
 
-Default workload: one Llama-7B-shaped MoE layer (T=2048 tokens, d=4096,
-E=8 experts, I=1376, bf16, Zipf(1.0) router bias).  Expert weights rotate
-through several packed copies so that every step reads them cold from HBM
-(their 277 MB would otherwise sit in the 256 MB last-level cache), as the
-layers of a real model stack do.
+Default workload: the expert-aware request batch (256 requests x 32 tokens,
+T=8192, d=8192, E=8 experts of intermediate width 3584, bf16, one given
+expert id per request), the largest configuration that fits one GPU.
+Expert weights rotate through several packed copies so that every step
+reads them cold from HBM, as the layers of a real model stack do.
 
 Prints ONE JSON line:  value = tokens per second through one MoE layer,
 plus a per-kernel breakdown from HIP events on the launch stream, the
-roofline of the dominant kernel and the CPU oracle's rate on a bounded
-sample (rank 0, one GPU).
+roofline of the dominant kernel (the gate/up GEMM, MFMA-bound here) and
+the CPU oracle's rate on a bounded sample (rank 0, one GPU).  Beside it
+the same line carries the metric's two halves, each from a short run of
+its own: "decode" (the 32-layer decode stack, 64 tokens, against HBM
+bandwidth) and "prefill" (the skewed 16-expert prefill layer's gate/up
+GEMM, T=16384, against the bf16 MFMA peak).
 
     python bench.py [--gpus 1] [--steps 100] [--warmup 10] [--workload NAME]
 """
@@ -46,7 +50,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="llama7b_layer", choices=sorted(wl.WORKLOADS))
+    ap.add_argument("--workload", default="wide_requests", choices=sorted(wl.WORKLOADS))
     ap.add_argument("--weight-copies", type=int, default=0,
                     help="packed weight copies to rotate (0 = enough for >= 1 GiB)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -57,6 +61,10 @@ def parse():
                          "fused into the two GEMMs")
     ap.add_argument("--gemm-tile", type=int, default=0,
                     help="force a grouped-GEMM tile configuration (0 = automatic)")
+    ap.add_argument("--no-side", action="store_true",
+                    help="skip the decode-stack and prefill lines measured beside the main one")
+    ap.add_argument("--side-steps", type=int, default=20,
+                    help="timed steps of each side line")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
@@ -105,7 +113,13 @@ class Path:
         import torch
 
         from paper_2410_19123_amd import _lib
-        from tests import _util as U
+
+        class U:  # host -> device copies of the seeded inputs
+            to_dev = staticmethod(_lib.to_device)
+
+            @staticmethod
+            def weights_to_dev(*ws):
+                return tuple(_lib.to_device(a) for a in ws)
 
         self.torch, self.w, self.lib = torch, w, _lib.load()
         dev = torch.device("cuda:0")
@@ -446,38 +460,47 @@ def cpu_baseline(w: wl.Workload, target_s: float) -> dict:
                       f"{total:.1f} s"}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}); "
-              "sharding across GPUs is described in the design notes, not measured.",
-              file=sys.stderr)
-        sys.exit(2)
+def roofline(w: wl.Workload, wk: dict, dom_all: np.ndarray, dom: str) -> dict:
+    """Roofline object of the dominant kernel from its launch durations (us):
+    algorithmic bytes or flops over the mean launch, against HBM or MFMA."""
+    dom_us = float(dom_all.mean())
+    t = dom_us * 1e-6
+    t_hbm = wk["bytes"] / (HBM_GBS * 1e9)
+    pk = MFMA_F32_TFLOPS if w.dtype == "f32" else MFMA_BF16_TFLOPS
+    t_mfma = wk["flops"] / (pk * 1e12)
+    if t_hbm >= t_mfma:
+        ach = wk["bytes"] / t / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_GBS, 4), "traffic": None}
+    else:
+        ach = wk["flops"] / t / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": pk, "unit": "TFLOP/s",
+                "frac": round(ach / pk, 4), "traffic": None}
+    roof["launch_us"] = round(dom_us, 2)
+    roof["launch_us_p10_p50_p90"] = [round(float(v), 2)
+                                     for v in np.percentile(dom_all, [10, 50, 90])]
+    roof["algorithmic_bytes"] = int(wk["bytes"])
+    roof["algorithmic_flops"] = wk["flops"]
+    return roof
+
+
+def run_workload(w: wl.Workload, K: int, W: int, fused: bool = True, copies: int = 0,
+                 sample_every: int = 8, breakdown: int = 20) -> dict:
+    """Times K steps of workload w after W warmup steps (inputs resident in
+    HBM, weights rotated over >= 1 GiB of packed copies).  Inside the timed
+    region only the dominant kernel is bracketed by HIP events, on every
+    sample_every-th step; a separate pass of `breakdown` steps then times
+    every call.  Returns the measurements and the path."""
     import torch
-    if not torch.cuda.is_available():
-        print("bench.py: no GPU visible", file=sys.stderr)
-        sys.exit(1)
 
-    w = wl.WORKLOADS[args.workload]
-    if (w.P or w.K > 1) and args.unfused:
-        print("bench.py: the permanent-expert and top-K workloads run the fused path only",
-              file=sys.stderr)
-        sys.exit(2)
     packed_bytes = 3 * (w.E + w.P // w.I) * (-(-w.I // 64) * 64) * w.d * w.elem_bytes
-    copies = args.weight_copies or max(4, -(-(1 << 30) // packed_bytes))
+    copies = copies or max(4, -(-(1 << 30) // packed_bytes))
     path = Path(w, copies)
-    if args.gemm_tile:
-        from paper_2410_19123_amd import _lib
-        _lib.readme_set_gemm_tile(args.gemm_tile)
-    K, W = args.steps, args.warmup
     ncopy = len(path.packed)
-
-    fused = not args.unfused
     names = [n for n, _ in path.calls(0, fused)]
     ev = {n: [] for n in names}
-
-    layers = w.layers
-    dom = "stack" if layers > 1 else "gate_up"
+    dom = "stack" if w.layers > 1 else "gate_up"
+    ev_dom = []
 
     def step(i, mode):
         """mode None: no events; "dom": an event pair around the dominant
@@ -502,28 +525,24 @@ def main():
                 nxt = marks[j + 1][1] if j + 1 < len(marks) else z
                 ev[n].append((a, nxt))
 
-    ev_dom = []
     for i in range(W):
         step(i, None)
     torch.cuda.synchronize()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     start.record()
-    # The dominant kernel's event pair goes on every 8th step of the timed
-    # region: a timing event pair costs ~4.5 us of a ~140 us step (measured
-    # with and without it), so sampling keeps the step time honest while the
-    # launch average still spans the whole region.
+    # The dominant kernel's event pair goes on every sample_every-th step of
+    # the timed region: an event pair costs a few us of the step, so sampling
+    # keeps the step time honest while the launch average still spans the
+    # whole region.
     for i in range(K):
-        step(W + i, "dom" if i % 8 == 0 else None)
+        step(W + i, "dom" if i % sample_every == 0 else None)
     stop.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gpu_ms = start.elapsed_time(stop)
-    ms_per_step = gpu_ms / K
     dom_all = np.array([1e3 * a.elapsed_time(b) for a, b in ev_dom])
-    dom_us = float(dom_all.mean())
-    # Per-call breakdown: a separate, shorter pass after the timed region.
-    for i in range(min(K, 20)):
+    for i in range(min(K, breakdown)):
         step(W + K + i, "all")
     torch.cuda.synchronize()
 
@@ -532,11 +551,12 @@ def main():
     offload = None
     if path.ex:
         hits, misses, nbytes = path.ex.stats()
-        steps_run = W + K + min(K, 20)
+        steps_run = W + K + min(K, breakdown)
+        ms = gpu_ms / K
         offload = {"slots": w.offload_slots, "policy": w.policy,
                    "hit_ratio": round(hits / max(hits + misses, 1), 4),
                    "gb_copied_per_step": round(nbytes / steps_run / 1e9, 3),
-                   "h2d_gb_s": round(nbytes / steps_run / (ms_per_step * 1e-3) / 1e9, 1)}
+                   "h2d_gb_s": round(nbytes / steps_run / (ms * 1e-3) / 1e9, 1)}
     if w.batching:
         # the batches differ from step to step: average their work
         per = [algorithmic(w, np.bincount(b, minlength=w.E), fused) for b in path.sched]
@@ -545,6 +565,58 @@ def main():
         counts = np.bincount(path.sched.reshape(-1), minlength=w.E) // path.sched.shape[0]
     kern_us = {n: (1e3 * float(np.mean([a.elapsed_time(b) for a, b in ev[n]])) if ev[n] else None)
                for n in names}
+    return dict(path=path, ncopy=ncopy, gpu_ms=gpu_ms, wall=wall, dom=dom, dom_all=dom_all,
+                counts=counts, work=work, kern_us=kern_us, offload=offload)
+
+
+def side_line(name: str, K: int, W: int) -> dict:
+    """One half of the metric measured beside the main line: the decode
+    stack's HBM fraction or the prefill gate/up's MFMA fraction."""
+    import torch
+    w = wl.WORKLOADS[name]
+    r = run_workload(w, K, W, sample_every=1, breakdown=0)
+    ms = r["gpu_ms"] / K
+    value = w.T * K / (r["gpu_ms"] / 1e3) * max(w.layers, 1)
+    roof = roofline(w, r["work"][r["dom"]], r["dom_all"], r["dom"])
+    roof["kernel"] = ("readme_moe_ffn_stack (all layers)" if w.layers > 1
+                      else "k_grouped_gemm (gate/up + SiLU*mul, rows gathered through perm)")
+    out = {"workload": name, "T": w.T, "d": w.d, "E": w.E, "I": w.I, "layers": w.layers,
+           "steps": K, "ms_per_step": round(ms, 4),
+           "tokens_per_s_per_layer": round(value, 1),
+           "tokens_per_expert": r["counts"].tolist(), "roofline": roof}
+    del r
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}); "
+              "sharding across GPUs is described in the design notes, not measured.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+
+    w = wl.WORKLOADS[args.workload]
+    if (w.P or w.K > 1) and args.unfused:
+        print("bench.py: the permanent-expert and top-K workloads run the fused path only",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.gemm_tile:
+        from paper_2410_19123_amd import _lib
+        _lib.load()
+        _lib.readme_set_gemm_tile(args.gemm_tile)
+    K, W = args.steps, args.warmup
+    fused = not args.unfused
+    r = run_workload(w, K, W, fused, args.weight_copies)
+    gpu_ms, dom, counts, work = r["gpu_ms"], r["dom"], r["counts"], r["work"]
+    ms_per_step = gpu_ms / K
+    layers = w.layers
 
     value = w.T * K / (gpu_ms / 1e3)  # tokens/s through one step
     if layers > 1:
@@ -553,32 +625,16 @@ def main():
     ffn_flops = 6.0 * rows * w.d * (w.I + w.P) * layers
 
     roof = None
-    if dom_us:
-        t = dom_us * 1e-6
-        wk = work[dom]
-        t_hbm = wk["bytes"] / (HBM_GBS * 1e9)
-        pk = MFMA_F32_TFLOPS if w.dtype == "f32" else MFMA_BF16_TFLOPS
-        t_mfma = wk["flops"] / (pk * 1e12)
-        if t_hbm >= t_mfma:
-            ach = wk["bytes"] / t / 1e9
-            roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_GBS, "unit": "GB/s",
-                    "frac": round(ach / HBM_GBS, 4), "traffic": None}
-        else:
-            ach = wk["flops"] / t / 1e12
-            roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": pk, "unit": "TFLOP/s",
-                    "frac": round(ach / pk, 4), "traffic": None}
+    if r["dom_all"].size:
+        roof = roofline(w, work[dom], r["dom_all"], dom)
         roof["kernel"] = ("readme_moe_ffn_stack (all layers)" if layers > 1
                           else "k_grouped_gemm (gate/up + SiLU*mul"
                           + (", permanent expert as extra row groups" if w.P else "")
                           + (f", top-{w.K} (token, slot) pairs" if w.K > 1 else "")
                           + (", rows gathered through perm)" if fused else ")"))
-        roof["launch_us"] = round(dom_us, 2)
-        roof["launch_us_p10_p50_p90"] = [round(float(v), 2)
-                                         for v in np.percentile(dom_all, [10, 50, 90])]
         if dom == "gate_up" and fused and not args.gemm_tile:
             roof["traffic"] = traffic_bytes(w.name)
-        roof["algorithmic_bytes"] = int(wk["bytes"])
-        roof["algorithmic_flops"] = wk["flops"]
+    kern_us = r["kern_us"]
 
     out = {
         "metric": "expert-FFN tokens/sec per MoE layer",
@@ -596,13 +652,13 @@ def main():
         "config": {"workload": w.name, "T": w.T, "d": w.d, "E": w.E, "I": w.I, "P": w.P, "K": w.K,
                    "gemm_tile": args.gemm_tile,
                    "row_moves": "separate" if args.unfused or layers > 1 else "fused into GEMMs",
-                   "layers": layers, "weight_copies_rotated": ncopy,
+                   "layers": layers, "weight_copies_rotated": r["ncopy"],
                    "tokens_per_expert": counts.tolist(),
                    **({"batching": w.batching, "pool": w.pool,
                        "unique_experts_per_batch": round(float(np.mean(
-                           [len(set(b.tolist())) for b in path.sched])), 2)}
+                           [len(set(b.tolist())) for b in r["path"].sched])), 2)}
                       if w.batching else {}),
-                   **({"offload": offload} if offload else {})},
+                   **({"offload": r["offload"]} if r["offload"] else {})},
         "ffn_tflops": round(ffn_flops / (ms_per_step * 1e-3) / 1e12, 2),
         # event pair before each call, from a separate 20-step pass after the
         # timed region (events between every call add their own gaps)
@@ -610,7 +666,7 @@ def main():
         # algorithmic bytes of each call over its breakdown time (HBM peak 8000 GB/s)
         "kernels_gbs": {k: round(work[k]["bytes"] / (v * 1e-6) / 1e9, 1)
                         for k, v in kern_us.items() if v and k in work},
-        "host_wall_ms_per_step": round(1e3 * wall / K, 4),
+        "host_wall_ms_per_step": round(1e3 * r["wall"] / K, 4),
         "roofline": roof,
     }
     if args.copy_probe:
@@ -620,6 +676,15 @@ def main():
             bb.copy_(a)
         torch.cuda.synchronize()
         out["copy_probe_bytes"] = 1 << 30
+        del a, bb
+    del r
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    # The metric's two halves beside the main line: % of HBM for the decode
+    # step (the 32-layer stack), % of the MFMA peak for the prefill gate/up.
+    if not args.no_side and args.workload not in ("llama7b_decode32", "prefill_skew16"):
+        out["decode"] = side_line("llama7b_decode32", args.side_steps, 3)
+        out["prefill"] = side_line("prefill_skew16", args.side_steps, 3)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(out), flush=True)

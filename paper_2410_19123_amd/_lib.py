@@ -421,6 +421,23 @@ def readme_combine_topk(y_pairs, weights, K, y=None):
 README_CACHE_POLICIES = {"belady": 0, "lru": 1, "fifo": 2, "random": 3}
 
 
+def to_device(a, device="cuda:0") -> torch.Tensor:
+    """Host array -> device tensor (uint16 arrays hold bf16 bit patterns)."""
+    import numpy as np
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+
+def from_device(t: torch.Tensor):
+    """Device tensor -> host array (bf16 as uint16 bit patterns)."""
+    t = t.detach().cpu()
+    if t.dtype == torch.bfloat16:
+        import numpy as np
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
+
+
 def _host_i32(a):
     import numpy as np
     a = np.ascontiguousarray(a, dtype=np.int32)

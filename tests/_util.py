@@ -19,16 +19,13 @@ def dev():
 
 
 def to_dev(a: np.ndarray) -> torch.Tensor:
-    if a.dtype == np.uint16:
-        return torch.from_numpy(a.view(np.int16)).to(dev()).view(torch.bfloat16)
-    return torch.from_numpy(np.ascontiguousarray(a)).to(dev())
+    from paper_2410_19123_amd import _lib
+    return _lib.to_device(a, dev())
 
 
 def from_dev(t: torch.Tensor) -> np.ndarray:
-    t = t.detach().cpu()
-    if t.dtype == torch.bfloat16:
-        return t.view(torch.int16).numpy().view(np.uint16)
-    return t.numpy()
+    from paper_2410_19123_amd import _lib
+    return _lib.from_device(t)
 
 
 def as_f64(a: np.ndarray) -> np.ndarray:
@@ -49,23 +46,6 @@ def close(got: np.ndarray, ref: np.ndarray, what: str = ""):
     assert max_rel <= MAX_REL, f"{what}: max rel err {max_rel:.3e}"
     assert l1 <= L1_REL, f"{what}: normalized L1 err {l1:.3e}"
     return max_rel, l1
-
-
-def sample_rows(offsets: np.ndarray, n_random: int, seed: int = 0) -> np.ndarray:
-    """Grouped rows to check at full size: the first two and last two rows of
-    every expert block (tile edges and ragged tails) plus random rows."""
-    rows = set()
-    E = offsets.shape[0] - 1
-    for e in range(E):
-        a, b = int(offsets[e]), int(offsets[e + 1])
-        for j in (a, a + 1, b - 2, b - 1):
-            if a <= j < b:
-                rows.add(j)
-    n = int(offsets[E])
-    if n:
-        rng = np.random.default_rng(seed)
-        rows.update(rng.integers(0, n, size=min(n_random, n)).tolist())
-    return np.array(sorted(rows), np.int64)
 
 
 def weights_to_dev(wg, wu, wd):
