@@ -68,6 +68,8 @@ typedef int32_t readme_dtype;
 
 #define README_MAX_EXPERTS 256
 #define README_MAX_PERMANENT_SLICES 16
+/* Size of the fixed device array readme_moe_ffn_fused_noalloc keeps h in. */
+#define README_NOALLOC_SCRATCH_BYTES (64ll << 20)
 
 /* Human-readable name of a status code (static storage). */
 const char *readme_status_string(readme_status s);
@@ -243,6 +245,29 @@ readme_status readme_moe_ffn_fused(readme_dtype dt, int64_t T, int64_t d,
                                    const void *packed, void *y,
                                    void *workspace, size_t workspace_bytes,
                                    void *stream);
+
+/*
+ * readme_moe_ffn_fused_noalloc -- readme_moe_ffn_fused for callers that
+ * cannot allocate device memory (work under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): no workspace argument.
+ * h lives in a file-scope device array of README_NOALLOC_SCRATCH_BYTES
+ * (64 MiB) that each GPU the library runs on holds until the process ends;
+ * its device address is looked up on the first call on the current device
+ * (the stream must belong to the current device).  The call allocates and
+ * frees nothing.  Same kernels, tiles and summation order as
+ * readme_moe_ffn_fused, so the same bits.
+ *   Arguments as readme_moe_ffn_fused without workspace.
+ * README_ERR_UNSUPPORTED if T * readme_padded_intermediate(I) * element
+ * size exceeds README_NOALLOC_SCRATCH_BYTES (checked before anything is
+ * enqueued).  All calls on one GPU share its array: calls that overlap on
+ * one GPU (other streams or host threads) race on h and give wrong
+ * results; the array keeps the last call's contents, which no call reads.
+ */
+readme_status readme_moe_ffn_fused_noalloc(readme_dtype dt, int64_t T, int64_t d,
+                                           int32_t E, int64_t I, const void *x,
+                                           const int32_t *perm,
+                                           const int32_t *offsets,
+                                           const void *packed, void *y, void *stream);
 
 /*
  * The two halves of readme_moe_ffn_fused:

@@ -42,6 +42,8 @@ SIGNATURES = {
     "readme_moe_gate_up": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P]),
     "readme_moe_ffn_fused": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _P, _SZ,
                                     _P]),
+    "readme_moe_ffn_fused_noalloc": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P,
+                                            _P]),
     "readme_moe_gate_up_gather": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _P]),
     "readme_moe_down_scatter": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _P]),
     "readme_moe_down": (_I32, [_I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P]),
@@ -234,6 +236,16 @@ def readme_moe_ffn_fused(x, perm, offsets, packed, E, I, y=None, workspace=None)
     _call("readme_moe_ffn_fused", _dt(x), T, d, E, I, _p(x), _p(perm), _p(offsets), _p(packed),
           _p(y), _p(workspace), workspace.numel() * workspace.element_size(),
           _stream(x.device))
+    return y
+
+
+def readme_moe_ffn_fused_noalloc(x, perm, offsets, packed, E, I, y):
+    """readme_moe_ffn_fused with h in the library's fixed device array (no
+    workspace); y (token order) must be given."""
+    T, d = x.shape
+    _dev(x, perm, offsets, packed, y)
+    _call("readme_moe_ffn_fused_noalloc", _dt(x), T, d, E, I, _p(x), _p(perm), _p(offsets),
+          _p(packed), _p(y), _stream(x.device))
     return y
 
 

@@ -196,3 +196,17 @@ def test_tile_override_is_per_thread(lib):
     assert lib.readme_get_gemm_tile() == 5
     assert lib.readme_set_gemm_tile(0) == 0
     assert lib.readme_get_gemm_tile() == 0
+
+
+def test_noalloc_size_limit(lib):
+    """The allocation-free FFN refuses an h larger than its fixed array
+    (64 MiB) on the host, before touching the device."""
+    f = lib.readme_moe_ffn_fused_noalloc
+    # T * padded(I) * 2 bytes: 2^19 * 64 * 2 = 64 MiB fits (then the NULL x
+    # is README_ERR_ARG); one more row does not.
+    assert f(1, 1 << 19, 64, 2, 64, None, None, None, None, None, None) == 1
+    assert f(1, (1 << 19) + 1, 64, 2, 64, None, None, None, None, None, None) == 2
+    assert f(0, 1 << 18, 64, 2, 64, None, None, None, None, None, None) == 1   # fp32: fits
+    assert f(0, (1 << 18) + 1, 64, 2, 64, None, None, None, None, None, None) == 2
+    assert f(1, 0, 64, 2, 64, None, None, None, None, None, None) == 0        # T = 0
+    assert f(1, 16, 4000, 2, 64, FAKE, FAKE, FAKE, FAKE, FAKE, None) == 2     # d % 64
