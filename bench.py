@@ -345,12 +345,14 @@ class Path:
 # exactly 1 GiB, factor 1).  Valid only for the sources the counters were taken
 # with: the entry carries their sha256 and is dropped (traffic null) once any of
 # them changes.
-TRAFFIC_SOURCES = ["csrc/gemm_kernels.hpp", "csrc/gemm.hip", "csrc/gemm_bf16_gate_up.hip",
-                   "csrc/common.hpp", "csrc/internal.hpp", "csrc/pack.hip", "workloads.py"]
+TRAFFIC_SOURCES = ["csrc/gemm_kernels.hpp", "csrc/gemm_mix.hpp", "csrc/gemm.hip",
+                   "csrc/gemm_mix_gate_up.hip", "csrc/common.hpp", "csrc/internal.hpp",
+                   "csrc/pack.hip", "workloads.py"]
 TRAFFIC = {
     # workload: (sources sha256, read bytes, written bytes) per gate/up launch
-    "llama7b_layer": ("ef8785fdcf3aa9a62c733a2897b35cebfb94a298f4e2362a408f00fc926fa712",
-                      234299094, 5767168),
+    # (profiles/traffic_gate_up_wide_requests.md)
+    "wide_requests": ("19077381f970b1286ab5f3cf1a4a410e855a15f4d457b126ce31d5a501247da5",
+                      2387195897, 58720256),
 }
 
 

@@ -2,7 +2,7 @@
 // in gemm_kernels.hpp, instantiated in gemm_f32.hip and gemm_bf16_*.hip.
 #include <limits.h>
 
-#include "gemm_kernels.hpp"
+#include "gemm_mix.hpp"
 
 namespace readme {
 
@@ -20,20 +20,20 @@ bool set_gemm_tile(int tile) {
 int get_gemm_tile() { return t_forced_tile; }
 
 // Tile shape by tokens per expert (the host knows T and E, not the split):
-// many rows per expert favour large tiles (fewer LDS and L2 bytes per
-// flop); few rows favour short tiles (no MFMA work on padding rows, more
-// workgroups to spread a weight stream over).  The 192-row register-streamed
-// tile has the fewest load bytes per MFMA, so it pays where each tile has a
-// long K loop and its tile count still fills the CUs evenly; the LDS
-// 256x256 tile keeps the count lowest, which matters when a partial round
-// of tiles would remain.  Thresholds come from tile sweeps on MI355X over
-// the Llama-7B-shaped layer (top-1, top-2, with a permanent expert), the
-// 16-expert prefill and the d = 8192 request batch.
+// many rows per expert favour tall tiles (fewer load bytes per flop); few
+// rows favour short tiles (no MFMA work on padding rows, more workgroups to
+// spread a weight stream over).  From the prefill shapes up, one launch
+// mixes tile heights (gemm_mix.hpp): each expert in full tiles of the
+// tallest height, its remainder in the shortest tile that holds it, the
+// tall tiles dispatched first -- this removes most padding rows and fills
+// the last round of the launch with short tiles.  Thresholds come from tile
+// sweeps on MI355X over the Llama-7B-shaped layer (top-1, top-2, with a
+// permanent expert), the 16-expert prefill and the d = 8192 request batch.
 static int tile_by_shape(bool f32, bool gate_up, const GemmArgs& g) {
     const int f = forced_tile();
     if (f > 0) return f;
     const int64_t per_expert = g.T / (g.E > 0 ? g.E : 1);
-    if (f32) {  // both operands through LDS (the register-streamed kernel is bf16 only)
+    if (f32) {  // both operands through LDS (the register-streamed kernels are bf16 only)
         if (per_expert >= (gate_up ? 768 : 192)) return TILE_256x256;
         return per_expert >= 96 && !gate_up ? TILE_128x256 : TILE_32x128;
     }
@@ -46,18 +46,20 @@ static int tile_by_shape(bool f32, bool gate_up, const GemmArgs& g) {
         return TILE_BD_32x128;
     }
     if (gate_up) {
-        if (per_expert >= 768) return g.K >= 8192 ? TILE_BD_192x256 : TILE_256x256;
+        if (per_expert >= 768) return TILE_MIX_256;
         // 128-row tiles while their estimated count (half a tile of padding
-        // per row group) fits one round on the chip's 256 CUs; past that the
-        // 256-row tile's single round wins (permanent-expert groups, top-K
-        // pairs).
+        // per row group) fits one round on the chip's 256 CUs, so that every
+        // CU streams; past that the mixed 256-row launch wins (permanent-
+        // expert groups: 401 estimated tiles, 142 -> 123 us).
         const int64_t groups = g.E + g.shared_groups;
         const int64_t rows = g.T * (1 + g.shared_groups);
         const int64_t est = (rows / 128 + groups / 2) * ceil_div(g.N, 256);
-        return est > 256 ? TILE_256x256 : TILE_BD_128x256;
+        return est > 256 ? TILE_MIX_256 : TILE_BD_128x256;
     }
-    if (g.K >= 1024) return TILE_BD_192x256_S2;
-    return per_expert >= 192 ? TILE_256x256 : TILE_128x256;
+    // Down: 192-row tiles with the remainders in shorter ones (request
+    // batch 553 -> 496 us, default layer 46.5 -> 44.6 us, skewed prefill
+    // 175 -> 172 us on one box).
+    return TILE_MIX_192;
 }
 
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s) {
@@ -68,6 +70,11 @@ hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s) {
     if (g.K >= (int64_t)32 << 16) return hipErrorInvalidValue;
     if (g.k_segs > 1 && epi != EPI_STORE) return hipErrorInvalidValue;  // segments: down only
     const int tile = tile_by_shape(f32, epi == EPI_GATE_UP_SILU, g);
+    if (!f32 && tile >= TILE_MIX_256) {
+        if (epi == EPI_GATE_UP_SILU) return launch_mix_bf16_gate_up(tile, g, s);
+        if (epi == EPI_RESID_ADD) return launch_mix_bf16_resid(tile, g, s);
+        return launch_mix_bf16_store(tile, g, s);
+    }
     if (f32) {
         if (epi == EPI_GATE_UP_SILU) return launch_tile_f32_gate_up(tile, g, s);
         return launch_tile_f32_store(tile, g, s);

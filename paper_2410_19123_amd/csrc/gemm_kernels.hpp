@@ -615,7 +615,8 @@ struct BdTile {
 
     // One output tile; lds holds LDS_SLOTS slots, crow BM entries.  Starts
     // and ends with a barrier, so consecutive tiles may reuse both.
-    __device__ static void run(const GemmArgs& g, const TileLoc& t, u32x4* lds, int32_t* crow) {
+    __device__ __forceinline__ static void run(const GemmArgs& g, const TileLoc& t, u32x4* lds,
+                                               int32_t* crow) {
     constexpr int WN = TN * 32, BN = NW * WN;
     constexpr int EPC = F32 ? 4 : 8;
     constexpr int BK = CPR * EPC;
@@ -860,7 +861,13 @@ enum TileCfg {
     TILE_BD_192x256 = 21,     // 4 waves of 192x64, 3 K-steps
     TILE_BD_192x256_S2 = 22,  // 4 waves of 192x64, 2 K-steps
     TILE_BD_32x64 = 23,       // 1 wave of 32x64, 6 K-steps
-    TILE_LAST = TILE_BD_32x64,
+    // Register-streamed tiles of several heights in one launch (bf16; see
+    // gemm_mix.hpp): each expert in full tiles of the first height, its
+    // remainder in the smallest class that holds it.
+    TILE_MIX_256 = 24,  // 256 (2 K-steps), 128, 64, 32 rows (4 K-steps)
+    TILE_MIX_192 = 25,  // 192 (2 K-steps), 128, 64, 32 rows
+    TILE_MIX_128 = 26,  // 128, 64, 32 rows (4 K-steps)
+    TILE_LAST = TILE_MIX_128,
 };
 
 // Launches one tile configuration (instantiated per element type and

@@ -48,6 +48,9 @@ struct GemmArgs {
     // the caller knows on the host (the tile choice then sees the split).
     int m_tiles32;
     int n_tiles, m_tiles_max; // filled by the launcher
+    // Tiles of several heights in one launch: the block range of class c is
+    // [mix_start[c], mix_start[c+1]) (filled by the launcher).
+    int mix_start[5];
 };
 
 hipError_t launch_route(readme_dtype dt, int64_t T, int64_t d, int E, const void* x,
