@@ -476,6 +476,143 @@ __global__ __launch_bounds__(512) void k_route_lds_f32w(int64_t T, int64_t d, in
     }
 }
 
+// Many tokens, 9..16 experts (bf16): four tokens per wave, all experts'
+// partial sums in registers, and the 64 lane partials of the 64 (token,
+// expert) pairs folded together.  The canonical fold adds lane l + off into
+// lane l for off = 32, 16, ..., 1; here, at the step of `off`, each lane keeps
+// the half of its pairs whose pair index agrees with the lane index in that
+// bit and adds the partner lane's (l ^ off) values for them, so after six
+// steps lane l holds pair l's sum, formed by the same additions (fp32
+// addition is commutative, so a + b and b + a are the same bits) -- one
+// exchange per pair instead of six.  The router matrix is staged in LDS;
+// token chunks are streamed one chunk ahead.  Same summation order as k_route.
+template <int CPL>
+__global__ __launch_bounds__(512) void k_route_fold16(int64_t T, int64_t d, int E, int tb,
+                                                      const void* __restrict__ x,
+                                                      const void* __restrict__ wr,
+                                                      const float* __restrict__ bias,
+                                                      int32_t* __restrict__ ids,
+                                                      float* __restrict__ logits) {
+    constexpr int R = 4, EP = 16;
+    __shared__ uint4 wl[131072 / 16];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int nchunks = (int)(d / 8);
+    const uint4* xq = reinterpret_cast<const uint4*>(x);
+    const int64_t tb0 = (int64_t)blockIdx.x * tb;
+    {
+        // Rows of experts E .. 15 are staged as zeros, so every expert slot
+        // is summed without a branch (their logits are never used).
+        const uint4* wq = reinterpret_cast<const uint4*>(wr);
+        const int n = E * nchunks, n16 = EP * nchunks;
+        constexpr int PER = 131072 / 16 / 512;
+#pragma unroll
+        for (int k0 = 0; k0 < PER; k0 += 8) {
+            uint4 tmp[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int i = (int)threadIdx.x + 512 * (k0 + k);
+                tmp[k] = i < n ? wq[i] : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int i = (int)threadIdx.x + 512 * (k0 + k);
+                if (i < n16) wl[i] = tmp[k];
+            }
+        }
+    }
+    __syncthreads();
+
+    for (int g = wave; g * R < tb; g += 8) {
+        const int64_t t0 = tb0 + (int64_t)g * R;
+        if (t0 >= T) break;
+        int64_t row[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) row[r] = (t0 + r < T ? t0 + r : T - 1) * nchunks;
+        auto load = [&](uint4 (&q)[R], int j) {
+            const int c = lane + 64 * j;
+#pragma unroll
+            for (int r = 0; r < R; ++r) q[r] = c < nchunks ? xq[row[r] + c] : make_uint4(0, 0, 0, 0);
+        };
+        float acc[R * EP];
+#pragma unroll
+        for (int p = 0; p < R * EP; ++p) acc[p] = 0.0f;
+        uint4 xa[R], xb[R];
+        load(xa, 0);
+#pragma unroll
+        for (int j = 0; j < CPL; ++j) {
+            // chunk j in xa (even j) or xb (odd j); the next one is requested first
+            uint4 (&cur)[R] = (j & 1) ? xb : xa;
+            uint4 (&nxt)[R] = (j & 1) ? xa : xb;
+            if (j + 1 < CPL) load(nxt, j + 1);
+            const int c = lane + 64 * j;
+            if (c < nchunks) {
+                float xv[R][8];
+#pragma unroll
+                for (int r = 0; r < R; ++r) Chunk<8>::unpack(cur[r], xv[r]);
+#pragma unroll
+                for (int e = 0; e < EP; ++e) {
+                    float wv[8];
+                    Chunk<8>::unpack(wl[e * nchunks + c], wv);
+#pragma unroll
+                    for (int r = 0; r < R; ++r)
+#pragma unroll
+                        for (int q = 0; q < 8; ++q)
+                            acc[r * EP + e] = __builtin_fmaf(xv[r][q], wv[q], acc[r * EP + e]);
+                }
+            }
+        }
+        // Fold: pair p = r * EP + e; after the step of `off` a lane keeps the
+        // pairs whose bit log2(off) equals its own.
+        auto fold_step = [&](auto half_c) {
+            constexpr int H = decltype(half_c)::value;  // pairs kept = H
+            const bool up = (lane & H) != 0;
+#pragma unroll
+            for (int i = 0; i < H; ++i) {
+                const float mine = up ? acc[H + i] : acc[i];
+                const float give = up ? acc[i] : acc[H + i];
+                const float got = __shfl_xor(give, H, 64);
+                acc[i] = mine + got;
+            }
+        };
+        fold_step(std::integral_constant<int, 32>{});
+        fold_step(std::integral_constant<int, 16>{});
+        fold_step(std::integral_constant<int, 8>{});
+        fold_step(std::integral_constant<int, 4>{});
+        fold_step(std::integral_constant<int, 2>{});
+        fold_step(std::integral_constant<int, 1>{});
+        // Lane l now holds pair l: token r = l / EP, expert e = l % EP.
+        const int r = lane / EP, e = lane % EP;
+        float logit = acc[0];
+        if (bias && e < E) logit = logit + bias[e];
+        if (logits && e < E && t0 + r < T) logits[(t0 + r) * E + e] = logit;
+        // First maximum in index order (strict >: ties to the lowest index,
+        // a NaN never wins), each lane scanning its token's E logits.
+        float best = __shfl(logit, r * EP, 64);
+        int bid = 0;
+        for (int k = 1; k < E; ++k) {
+            const float v = __shfl(logit, r * EP + k, 64);
+            if (v > best) {
+                best = v;
+                bid = k;
+            }
+        }
+        if (e == 0 && t0 + r < T) ids[t0 + r] = bid;
+    }
+}
+
+template <int CPL>
+static hipError_t launch_route_fold16(int64_t T, int64_t d, int E, const void* x, const void* w,
+                                      const float* bias, int32_t* ids, float* logits,
+                                      hipStream_t s) {
+    int64_t tb = ceil_div(T, 256);
+    tb = tb < 8 ? 8 : (tb > 128 ? 128 : tb);
+    tb = round_up(tb, 4);
+    k_route_fold16<CPL><<<dim3((unsigned)ceil_div(T, tb)), dim3(512), 0, s>>>(
+        T, d, E, (int)tb, x, w, bias, ids, logits);
+    return hipGetLastError();
+}
+
 template <int R, int CPL, int W, int LDS_BYTES>
 static hipError_t launch_route_lds_r(int64_t T, int64_t d, int E, const void* x, const void* w,
                                      const float* bias, int32_t* ids, float* logits,
@@ -579,6 +716,17 @@ hipError_t launch_route(readme_dtype dt, int64_t T, int64_t d, int E, const void
             if (dt == README_BF16)
                 return launch_route_lds<8, 65536>(cpl, T, d, E, x, w, bias, ids, logits, s);
             return launch_route_lds<4, 65536>(cpl, T, d, E, x, w, bias, ids, logits, s);
+        }
+        // Many tokens, 9..16 experts: the folded kernel (16 router rows,
+        // zero-padded past E, in LDS).
+        if (dt == README_BF16 && E > 8 && E <= 16 && 16 * d * 2 <= 131072 && T >= 8192) {
+            switch (cpl) {
+                case 1: return launch_route_fold16<1>(T, d, E, x, w, bias, ids, logits, s);
+                case 2: return launch_route_fold16<2>(T, d, E, x, w, bias, ids, logits, s);
+                case 4: return launch_route_fold16<4>(T, d, E, x, w, bias, ids, logits, s);
+                case 8: return launch_route_fold16<8>(T, d, E, x, w, bias, ids, logits, s);
+                default: break;
+            }
         }
         if (wbytes <= 131072 && T >= 8192) {
             if (dt == README_BF16)
