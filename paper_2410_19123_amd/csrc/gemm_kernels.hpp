@@ -407,6 +407,59 @@ struct Epilogue {
     }
 };
 
+// Gate/up epilogue when every wave holds a single 32-column group (one
+// wave per 32-row weight group): the gate columns of neuron group n are in
+// wave 2n, the up columns in wave 2n+1, so the pair meets in LDS.  The
+// waves put their fp32 sums into a row-major LDS tile, then all threads form
+// h = silu(g) * u for 8 neurons at a time and store whole output rows with
+// 16-byte stores (same fp32 arithmetic as Epilogue, so the same bits).
+template <int TM, int NW>
+struct EpiloguePairWaves {
+    using OT = uint16_t;
+    static constexpr int LDF = NW * 32 + 4;                  // fp32 row pitch
+    static constexpr int LDS_BYTES = TM * 32 * LDF * 4;
+    static constexpr int PER_ROW = NW * 2;                   // 8-neuron pieces per row
+    static_assert(NW % 2 == 0, "gate and up waves come in pairs");
+
+    __device__ static void run(const GemmArgs& g, const f32x16 (&acc)[TM][1], int wm, int wn,
+                               int64_t n0, int rows, int64_t m0, const int32_t* crow,
+                               void* lds_raw, int tid, int nthreads) {
+        (void)wm;
+        float* L = reinterpret_cast<float*>(lds_raw);
+        const int lane = tid & 63;
+        __syncthreads();  // LDS free (K loop done)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int lr = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                L[lr * LDF + wn * 32 + (lane & 31)] = acc[i][0][r];
+            }
+        __syncthreads();
+        const int64_t oc0 = n0 / 2, n_out = g.N / 2;
+        for (int u = tid; u < TM * 32 * PER_ROW; u += nthreads) {
+            const int rt = u / PER_ROW, pc = u - rt * PER_ROW;
+            if (rt >= rows) continue;
+            const int64_t col = oc0 + (int64_t)pc * 8;
+            if (col >= n_out) continue;
+            const int64_t grow = g.c_rows ? (int64_t)crow[rt] : m0 + rt;
+            if (grow < 0 || grow >= g.T) continue;
+            const int ng = pc / 4, w0 = (pc % 4) * 8;    // neuron group, first neuron in it
+            const float* gt = L + rt * LDF + (2 * ng) * 32 + w0;
+            const float* up = L + rt * LDF + (2 * ng + 1) * 32 + w0;
+            uint32_t packed[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t lo = f32_to_bf16(silu_f32(gt[2 * k]) * up[2 * k]);
+                const uint32_t hi = f32_to_bf16(silu_f32(gt[2 * k + 1]) * up[2 * k + 1]);
+                packed[k] = lo | (hi << 16);
+            }
+            const u32x4 v = {packed[0], packed[1], packed[2], packed[3]};
+            *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(g.C) + grow * g.ldc + col) = v;
+        }
+    }
+};
+
 template <int BM, int BN, int WGM, int WGN, int NSTAGE, bool F32, int EPI, int KC = CPR>
 __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs args) {
     constexpr int NW = WGM * WGN;
@@ -609,7 +662,10 @@ template <int BM, int NW, int TN, int S, bool F32, int EPI>
 struct BdTile {
     static constexpr int TM = BM / 32;
     static constexpr int STAGE = BM * CPR;  // u32x4 slots per LDS buffer
-    using Epi = Epilogue<TM, TN, 1, NW, F32, EPI, 73728>;
+    // One 32-column group per wave: gate and up meet across waves.
+    using Epi = std::conditional_t<(EPI == EPI_GATE_UP_SILU && TN == 1 && !F32),
+                                   EpiloguePairWaves<TM, NW>,
+                                   Epilogue<TM, TN, 1, NW, F32, EPI, 73728>>;
     static constexpr int LDS_SLOTS =
         2 * STAGE > Epi::LDS_BYTES / 16 ? 2 * STAGE : Epi::LDS_BYTES / 16;
 
@@ -623,7 +679,8 @@ struct BdTile {
     constexpr int ESZ = F32 ? 4 : 2;
     constexpr int A_INS = BM / 8 / NW;    // activation loads per wave per K-step
     static_assert(BM % 32 == 0 && A_INS * 8 * NW == BM, "activation split");
-    static_assert(EPI != EPI_GATE_UP_SILU || TN % 2 == 0, "gate/up pairs");
+    static_assert(EPI != EPI_GATE_UP_SILU || TN % 2 == 0 || (TN == 1 && NW % 2 == 0 && !F32),
+                  "gate/up pairs");
     static_assert(S >= 2, "stages");
 
     const int tid = threadIdx.x;
@@ -867,7 +924,12 @@ enum TileCfg {
     TILE_MIX_256 = 24,  // 256 (2 K-steps), 128, 64, 32 rows (4 K-steps)
     TILE_MIX_192 = 25,  // 192 (2 K-steps), 128, 64, 32 rows
     TILE_MIX_128 = 26,  // 128, 64, 32 rows (4 K-steps)
-    TILE_LAST = TILE_MIX_128,
+    // Register-streamed 32 x 128 with four waves of one 32-column weight
+    // group each (gate and up paired across waves in the epilogue):
+    TILE_BD_32x128_W4 = 27,     // 6 K-steps in flight
+    TILE_BD_32x128_W4_S8 = 28,  // 8 K-steps in flight
+    TILE_BD_32x128_W4_S4 = 29,  // 4 K-steps in flight
+    TILE_LAST = TILE_BD_32x128_W4_S4,
 };
 
 // Launches one tile configuration (instantiated per element type and
@@ -901,6 +963,9 @@ hipError_t launch_tile(int tile, GemmArgs g, hipStream_t s) {
             case TILE_BD_192x256: return launch_bd<192, 4, 2, 3, F32, EPI>(g, s);
             case TILE_BD_192x256_S2: return launch_bd<192, 4, 2, 2, F32, EPI>(g, s);
             case TILE_BD_32x64: return launch_bd<32, 1, 2, 6, F32, EPI>(g, s);
+            case TILE_BD_32x128_W4: return launch_bd<32, 4, 1, 6, F32, EPI>(g, s);
+            case TILE_BD_32x128_W4_S8: return launch_bd<32, 4, 1, 8, F32, EPI>(g, s);
+            case TILE_BD_32x128_W4_S4: return launch_bd<32, 4, 1, 4, F32, EPI>(g, s);
             default: break;
         }
     }
