@@ -58,10 +58,11 @@ static int tile_by_shape(bool f32, bool gate_up, const GemmArgs& g) {
         const int64_t est = (rows / 128 + groups / 2) * ceil_div(g.N, 256);
         return est > 256 ? TILE_MIX_256 : TILE_BD_128x256;
     }
-    // Down: 192-row tiles with the remainders in shorter ones (request
-    // batch 553 -> 496 us, default layer 46.5 -> 44.6 us, skewed prefill
-    // 175 -> 172 us on one box).
-    return TILE_MIX_192;
+    // Down: 192-row register-streamed tiles.  From 768 rows per expert one
+    // height (interleaved same-box runs: request batch 505 vs 510 us mixed,
+    // skewed prefill 172 vs 176 us); below, the remainders in shorter tiles
+    // (default layer 46.5 -> 44.6 us).
+    return per_expert >= 768 ? TILE_BD_192x256_S2 : TILE_MIX_192;
 }
 
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s) {
