@@ -341,18 +341,26 @@ class Path:
 # HBM traffic of the dominant kernel, per launch, from two rocprofv3 --pmc runs of
 # this script (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each scaled by what
 # the same counter reads for a plain 1 GiB device copy in the same run (--copy-probe:
-# FETCH_SIZE reads about 524,310 KiB for it, so reads scale by about 1.9999; WRITE_SIZE reads
-# exactly 1 GiB, factor 1).  Valid only for the sources the counters were taken
-# with: the entry carries their sha256 and is dropped (traffic null) once any of
+# FETCH_SIZE reads about 524,308 KiB for it, so reads scale by about 1.99992; WRITE_SIZE
+# reads exactly 1 GiB, factor 1).  Valid only for the sources the counters were taken
+# with: each entry carries their sha256 and is dropped (traffic null) once any of
 # them changes.
-TRAFFIC_SOURCES = ["csrc/gemm_kernels.hpp", "csrc/gemm_mix.hpp", "csrc/gemm.hip",
-                   "csrc/gemm_mix_gate_up.hip", "csrc/common.hpp", "csrc/internal.hpp",
-                   "csrc/pack.hip", "workloads.py"]
+_GEMM_SOURCES = ["csrc/gemm_kernels.hpp", "csrc/gemm_mix.hpp", "csrc/gemm.hip",
+                 "csrc/gemm_mix_gate_up.hip", "csrc/common.hpp", "csrc/internal.hpp",
+                 "csrc/pack.hip", "workloads.py"]
+_STACK_SOURCES = ["csrc/gemm_kernels.hpp", "csrc/gemm.hip", "csrc/gemm_bf16_gate_up.hip",
+                  "csrc/gemm_bf16_resid.hip", "csrc/norm.hip", "csrc/abi.hip",
+                  "csrc/common.hpp", "csrc/internal.hpp", "csrc/pack.hip", "workloads.py"]
 TRAFFIC = {
-    # workload: (sources sha256, read bytes, written bytes) per gate/up launch
-    # (profiles/traffic_gate_up_wide_requests.md)
-    "wide_requests": ("19077381f970b1286ab5f3cf1a4a410e855a15f4d457b126ce31d5a501247da5",
-                      2387195897, 58720256),
+    # workload: (sources, their sha256, read bytes, written bytes) per launch of the
+    # dominant call: the gate/up GEMM (profiles/traffic_gate_up_wide_requests.md), or
+    # the whole 32-layer stack (profiles/traffic_stack_llama7b_decode32.md)
+    "wide_requests": (_GEMM_SOURCES,
+                      "ddec437c0077649ec40cc55b08109983f4f3da5364293d942b91b471a132ab4c",
+                      2390474612, 58720256),
+    "llama7b_decode32": (_STACK_SOURCES,
+                         "82194f173573adb9f1ed7ec71ffb323ab519ff6164d8a95cb4a4e0b657dbe1d7",
+                         7873825371, 56098816),
 }
 
 
@@ -361,14 +369,15 @@ def traffic_bytes(workload: str):
     if entry is None:
         return None
     import hashlib
+    sources, sha, rd, wr = entry
     root = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2410_19123_amd")
     h = hashlib.sha256()
-    for rel in TRAFFIC_SOURCES:
+    for rel in sources:
         with open(os.path.join(root, rel), "rb") as f:
             h.update(f.read())
-    if h.hexdigest() != entry[0]:
+    if h.hexdigest() != sha:
         return None
-    return entry[1] + entry[2]
+    return rd + wr
 
 
 def algorithmic(w: wl.Workload, counts: np.ndarray, fused: bool = False) -> dict:
@@ -580,6 +589,7 @@ def side_line(name: str, K: int, W: int) -> dict:
     ms = r["gpu_ms"] / K
     value = w.T * K / (r["gpu_ms"] / 1e3) * max(w.layers, 1)
     roof = roofline(w, r["work"][r["dom"]], r["dom_all"], r["dom"])
+    roof["traffic"] = traffic_bytes(name)
     roof["kernel"] = ("readme_moe_ffn_stack (all layers)" if w.layers > 1
                       else "k_grouped_gemm (gate/up + SiLU*mul, rows gathered through perm)")
     out = {"workload": name, "T": w.T, "d": w.d, "E": w.E, "I": w.I, "layers": w.layers,
@@ -634,7 +644,7 @@ def main():
                           + (", permanent expert as extra row groups" if w.P else "")
                           + (f", top-{w.K} (token, slot) pairs" if w.K > 1 else "")
                           + (", rows gathered through perm)" if fused else ")"))
-        if dom == "gate_up" and fused and not args.gemm_tile:
+        if not args.gemm_tile and (dom == "stack" or fused):
             roof["traffic"] = traffic_bytes(w.name)
     kern_us = r["kern_us"]
 
