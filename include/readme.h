@@ -556,6 +556,35 @@ readme_status readme_ungroup(readme_dtype dt, int64_t T, int64_t d,
                              void *y, void *stream);
 
 /*
+ * The softmax-weighted top-1 variant of Eq. 2.  Eq. 2 multiplies each
+ * selected expert's output by its gate value G(x)_i, and Eq. 4 applies a
+ * softmax to G; the main path takes the top-1 output unweighted (so E = 1
+ * is the dense FFN).  These two calls give the weighted form instead:
+ *
+ * readme_gate_weights -- for every token t with 0 <= expert_ids[t] < E and
+ *   inv_perm[t] >= 0:  row_scale[inv_perm[t]] = p_t, the softmax of the
+ *   token's logits at its expert,
+ *     p_t = exp(l[t][e_t] - m_t) / sum_e exp(l[t][e] - m_t),  m_t = max_e l[t][e],
+ *   in fp32 with the sum in ascending e (grouped order, ready for
+ *   readme_ungroup_scaled).  Other entries of row_scale are not written.
+ *   logits [T][E] fp32 (readme_route's), expert_ids [T], inv_perm [T] int32
+ *   (readme_group_by_expert's), row_scale [T] fp32 out.  Finite logits are
+ *   assumed (a NaN or +inf logit makes p_t NaN).
+ *
+ * readme_ungroup_scaled -- readme_ungroup with a weight per grouped row:
+ *   y[t] = y_grouped[j] * row_scale[j], j = inv_perm[t], the product taken
+ *   in fp32 and rounded once to dt; a zero row where j < 0.
+ *   y_grouped [T][d] dt, inv_perm [T] int32, row_scale [T] fp32 (grouped
+ *   order), y [T][d] dt out.  Requires d * element size a multiple of 16.
+ */
+readme_status readme_gate_weights(int64_t T, int32_t E, const float *logits,
+                                  const int32_t *expert_ids, const int32_t *inv_perm,
+                                  float *row_scale, void *stream);
+readme_status readme_ungroup_scaled(readme_dtype dt, int64_t T, int64_t d,
+                                    const void *y_grouped, const int32_t *inv_perm,
+                                    const float *row_scale, void *y, void *stream);
+
+/*
  * readme_moe_ffn_stack -- L stacked MoE layers of one decode or prefill step,
  * run in grouped order.  The router runs once and a token's expert is the
  * same at every layer (Sec. 2.3 and Sec. 4.2), so grouping is done once and

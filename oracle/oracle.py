@@ -270,6 +270,42 @@ def f32_to_bf16(a: np.ndarray) -> np.ndarray:
     return out
 
 
+def gate_weights(logits: np.ndarray, ids: np.ndarray) -> np.ndarray:
+    """Gate value of each token's expert under a softmax over the router's
+    logits (Eq. 2's factor G(x)_i with Eq. 4's softmax applied to G): the
+    weighted top-1 variant, p_t = softmax(logits[t])[ids[t]], in fp64 on the
+    fp32 logits.  NaN for tokens whose id is outside [0, E)."""
+    lg = np.asarray(logits, np.float32).astype(np.float64)
+    T, E = lg.shape
+    ids = np.asarray(ids, np.int64)
+    out = np.full(T, np.nan)
+    for t in range(T):
+        e = int(ids[t])
+        if 0 <= e < E:
+            z = np.exp(lg[t] - lg[t].max())
+            out[t] = z[e] / z.sum()
+    return out
+
+
+def ungroup_scaled(y_g: np.ndarray, inv_perm: np.ndarray, row_scale: np.ndarray) -> np.ndarray:
+    """y[t] = y_g[j] * row_scale[j], j = inv_perm[t]: the product of the
+    element (exact in fp32) and the fp32 weight, rounded to fp32 (IEEE) and
+    then to the element type (bf16: round to nearest even); zero rows where
+    j < 0.  bf16 arrays are uint16 bit patterns."""
+    inv = np.asarray(inv_perm, np.int64)
+    scale = np.asarray(row_scale, np.float32)
+    bf16 = y_g.dtype == np.uint16
+    vals = (y_g.astype(np.uint32) << 16).view(np.float32) if bf16 else y_g.astype(np.float32)
+    out = np.zeros(y_g.shape, np.float32)
+    ok = inv >= 0
+    out[ok] = vals[inv[ok]] * scale[inv[ok]][:, None]
+    if bf16:
+        res = f32_to_bf16(out)
+        res[~ok] = 0
+        return res
+    return out
+
+
 def full_path(x, w_router, bias, w_gate, w_up, w_down, ids=None, permanent=None):
     """route -> group -> gather -> expert FFN -> ungroup, one layer.
 

@@ -75,6 +75,8 @@ SIGNATURES = {
     "readme_offload_plan": (_I32, [_I32, _I32, _I32, _I32, _I32, _P, _I32, _I64, _P, _P, _P,
                                    _P]),
     "readme_ungroup": (_I32, [_I32, _I64, _I64, _P, _P, _P, _P]),
+    "readme_gate_weights": (_I32, [_I64, _I32, _P, _P, _P, _P, _P]),
+    "readme_ungroup_scaled": (_I32, [_I32, _I64, _I64, _P, _P, _P, _P, _P]),
     "readme_moe_ffn_stack_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
     "readme_moe_ffn_stack": (_I32, [_I64, _I64, _I32, _I64, _I32, _P, _P, _P, _F, _P,
                                     _SZ, _P]),
@@ -570,6 +572,28 @@ class Offload:
             self.close()
         except Exception:
             pass
+
+
+def readme_gate_weights(logits, expert_ids, inv_perm, row_scale=None):
+    """Softmax gate of each routed token at its expert, in grouped order."""
+    T, E = logits.shape
+    if row_scale is None:
+        row_scale = torch.zeros(T, dtype=torch.float32, device=logits.device)
+    _dev(logits, expert_ids, inv_perm, row_scale)
+    _call("readme_gate_weights", T, E, _p(logits), _p(expert_ids), _p(inv_perm), _p(row_scale),
+          _stream(logits.device))
+    return row_scale
+
+
+def readme_ungroup_scaled(y_grouped, inv_perm, row_scale, y=None):
+    """Rows back to token order, each scaled by its grouped row's weight."""
+    T, d = y_grouped.shape
+    if y is None:
+        y = torch.empty_like(y_grouped)
+    _dev(y_grouped, inv_perm, row_scale, y)
+    _call("readme_ungroup_scaled", _dt(y_grouped), T, d, _p(y_grouped), _p(inv_perm),
+          _p(row_scale), _p(y), _stream(y_grouped.device))
+    return y
 
 
 def readme_ungroup(y_grouped, inv_perm, y=None):

@@ -443,6 +443,29 @@ readme_status readme_ungroup(readme_dtype dt, int64_t T, int64_t d, const void* 
                                        as_stream(stream)));
 }
 
+readme_status readme_gate_weights(int64_t T, int32_t E, const float* logits,
+                                  const int32_t* expert_ids, const int32_t* inv_perm,
+                                  float* row_scale, void* stream) {
+    if (T < 0) return README_ERR_ARG;
+    if (!experts_ok(E) || T > INT32_MAX) return README_ERR_UNSUPPORTED;
+    if (T == 0) return README_OK;
+    if (!logits || !expert_ids || !inv_perm || !row_scale) return README_ERR_ARG;
+    return hip_status(
+        launch_gate_weights(T, E, logits, expert_ids, inv_perm, row_scale, as_stream(stream)));
+}
+
+readme_status readme_ungroup_scaled(readme_dtype dt, int64_t T, int64_t d, const void* y_grouped,
+                                    const int32_t* inv_perm, const float* row_scale, void* y,
+                                    void* stream) {
+    if (!dtype_ok(dt) || T < 0 || d <= 0) return README_ERR_ARG;
+    if (T > INT32_MAX || (d * (int64_t)dtype_size(dt)) % 16 != 0) return README_ERR_UNSUPPORTED;
+    if (T == 0) return README_OK;
+    if (!y_grouped || !inv_perm || !row_scale || !y) return README_ERR_ARG;
+    if (!a16(y_grouped) || !a16(y)) return README_ERR_ARG;
+    return hip_status(launch_scale_rows(dt == README_F32, T, d * (int64_t)dtype_size(dt),
+                                        y_grouped, inv_perm, row_scale, T, y, as_stream(stream)));
+}
+
 size_t readme_moe_ffn_stack_workspace_bytes(int64_t T, int64_t d, int64_t I) {
     if (T < 0 || d <= 0 || I < 1) return 0;
     return (size_t)T * d * 2 + (size_t)T * padded_I(I) * 2;

@@ -63,6 +63,60 @@ __global__ __launch_bounds__(256) void k_move_rows(int64_t nrows, int64_t row_ch
     }
 }
 
+// Scaled ungroup: dst[r] = round(src[idx[r]] * scale[idx[r]]), the product
+// in fp32 and rounded once to the element type (zero row if idx[r] < 0).
+// One thread per 16-byte piece of an output row.
+template <bool F32>
+__global__ __launch_bounds__(256) void k_scale_rows(int64_t nrows, int64_t pieces,
+                                                    const uint4* __restrict__ src,
+                                                    const int32_t* __restrict__ idx,
+                                                    const float* __restrict__ scale,
+                                                    int64_t src_rows, uint4* __restrict__ dst) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= nrows * pieces) return;
+    const int64_t r = i / pieces, c = i - r * pieces;
+    const int32_t s = idx[r];
+    uint4 o = make_uint4(0, 0, 0, 0);
+    if (s >= 0 && s < src_rows) {
+        const uint4 v = src[(int64_t)s * pieces + c];
+        const float f = scale[s];
+        if constexpr (F32) {
+            o.x = __float_as_uint(__uint_as_float(v.x) * f);
+            o.y = __float_as_uint(__uint_as_float(v.y) * f);
+            o.z = __float_as_uint(__uint_as_float(v.z) * f);
+            o.w = __float_as_uint(__uint_as_float(v.w) * f);
+        } else {
+            auto two = [&](uint32_t w) {
+                const uint32_t lo = f32_to_bf16(bf16_lo(w) * f);
+                const uint32_t hi = f32_to_bf16(bf16_hi(w) * f);
+                return lo | (hi << 16);
+            };
+            o.x = two(v.x);
+            o.y = two(v.y);
+            o.z = two(v.z);
+            o.w = two(v.w);
+        }
+    }
+    dst[r * pieces + c] = o;
+}
+
+hipError_t launch_scale_rows(bool f32, int64_t nrows, int64_t row_bytes, const void* src,
+                             const int32_t* idx, const float* scale, int64_t src_rows, void* dst,
+                             hipStream_t s) {
+    const int64_t pieces = row_bytes / 16;
+    const int64_t blocks = ceil_div(nrows * pieces, 256);
+    if (blocks == 0) return hipSuccess;
+    if (f32)
+        k_scale_rows<true><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(
+            nrows, pieces, reinterpret_cast<const uint4*>(src), idx, scale, src_rows,
+            reinterpret_cast<uint4*>(dst));
+    else
+        k_scale_rows<false><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(
+            nrows, pieces, reinterpret_cast<const uint4*>(src), idx, scale, src_rows,
+            reinterpret_cast<uint4*>(dst));
+    return hipGetLastError();
+}
+
 hipError_t launch_move_rows(int64_t nrows, int64_t row_bytes, const void* src, const int32_t* idx,
                             int64_t src_rows, void* dst, hipStream_t s) {
     constexpr int ROWS = 8;

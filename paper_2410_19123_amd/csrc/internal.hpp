@@ -79,6 +79,11 @@ bool set_gemm_tile(int tile);
 int get_gemm_tile();
 hipError_t launch_topk(int64_t T, int E, int K, const float* logits, int32_t* ids, float* weights,
                        hipStream_t s);
+hipError_t launch_gate_weights(int64_t T, int E, const float* logits, const int32_t* ids,
+                               const int32_t* inv_perm, float* row_scale, hipStream_t s);
+hipError_t launch_scale_rows(bool f32, int64_t nrows, int64_t row_bytes, const void* src,
+                             const int32_t* idx, const float* scale, int64_t src_rows, void* dst,
+                             hipStream_t s);
 hipError_t launch_combine(bool f32, int64_t T, int64_t d, int K, const void* y_pairs,
                           const float* weights, void* y, hipStream_t s);
 hipError_t launch_rms_to_bf16(int64_t T, int64_t d, const float* x, const int32_t* offsets, int E,

@@ -53,6 +53,35 @@ hipError_t launch_topk(int64_t T, int E, int K, const float* logits, int32_t* id
     return hipGetLastError();
 }
 
+// Gate weight of a top-1 token, the softmax of its logits at its expert:
+// p_t = exp(l[t,e_t] - m_t) / sum_e exp(l[t,e] - m_t), m_t = max_e l[t,e],
+// fp32 with the experts in ascending order; written in grouped order,
+// row_scale[inv_perm[t]], for routed tokens only.  One thread per token.
+__global__ __launch_bounds__(256) void k_gate_weights(int64_t T, int E,
+                                                      const float* __restrict__ logits,
+                                                      const int32_t* __restrict__ ids,
+                                                      const int32_t* __restrict__ inv_perm,
+                                                      float* __restrict__ row_scale) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= T) return;
+    const int e_t = ids[t];
+    const int32_t j = inv_perm[t];
+    if (e_t < 0 || e_t >= E || j < 0) return;
+    const float* l = logits + t * E;
+    float m = l[0];
+    for (int e = 1; e < E; ++e) m = fmaxf(m, l[e]);
+    float sum = 0.0f;
+    for (int e = 0; e < E; ++e) sum += expf(l[e] - m);
+    row_scale[j] = expf(l[e_t] - m) / sum;
+}
+
+hipError_t launch_gate_weights(int64_t T, int E, const float* logits, const int32_t* ids,
+                               const int32_t* inv_perm, float* row_scale, hipStream_t s) {
+    const unsigned blocks = (unsigned)ceil_div(T, 256);
+    k_gate_weights<<<dim3(blocks), dim3(256), 0, s>>>(T, E, logits, ids, inv_perm, row_scale);
+    return hipGetLastError();
+}
+
 // y[t] = sum over slots k = 0 .. K-1 of w[t,k] * y_pairs[t*K + k], in fp32
 // in slot order, rounded once.  Each thread owns one 16-byte piece of a
 // token's row; the K pair rows of a token are adjacent in memory.

@@ -210,3 +210,16 @@ def test_noalloc_size_limit(lib):
     assert f(0, (1 << 18) + 1, 64, 2, 64, None, None, None, None, None, None) == 2
     assert f(1, 0, 64, 2, 64, None, None, None, None, None, None) == 0        # T = 0
     assert f(1, 16, 4000, 2, 64, FAKE, FAKE, FAKE, FAKE, FAKE, None) == 2     # d % 64
+
+
+def test_weighted_top1_argument_errors(lib):
+    g = lib.readme_gate_weights
+    assert g(-1, 8, FAKE, FAKE, FAKE, FAKE, None) == 1
+    assert g(16, 0, FAKE, FAKE, FAKE, FAKE, None) == 2
+    assert g(16, 8, None, FAKE, FAKE, FAKE, None) == 1
+    assert g(0, 8, None, None, None, None, None) == 0
+    u = lib.readme_ungroup_scaled
+    assert u(1, 16, 4, FAKE, FAKE, FAKE, FAKE, None) == 2          # 8-byte rows
+    assert u(1, 16, 64, FAKE, FAKE, None, FAKE, None) == 1         # no scale
+    assert u(1, 16, 64, ctypes.c_void_p(4104), FAKE, FAKE, FAKE, None) == 1  # misaligned
+    assert u(1, 0, 64, None, None, None, None, None) == 0
