@@ -65,6 +65,9 @@ def parse():
                     help="skip the decode-stack and prefill lines measured beside the main one")
     ap.add_argument("--side-steps", type=int, default=20,
                     help="timed steps of each side line")
+    ap.add_argument("--library-gemm", action="store_true",
+                    help="also time the same per-expert GEMMs with torch's library GEMM "
+                         "(context for the grouped kernels; not part of the path)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
@@ -580,6 +583,49 @@ def run_workload(w: wl.Workload, K: int, W: int, fused: bool = True, copies: int
                 counts=counts, work=work, kern_us=kern_us, offload=offload)
 
 
+def library_gemm(w: wl.Workload, counts: np.ndarray, reps: int = 10) -> dict:
+    """The workload's expert GEMMs run one expert at a time through torch's
+    library GEMM (hipBLASLt on ROCm), bf16 in, fp32 accumulation: gate and
+    up as one [T_e, d] x [d, 2I] product, down as [T_e, I] x [I, d].
+    Weights rotate over two copies; timed with events around all experts.
+    Context only: the SiLU*mul, the row gather and the scatter are left out,
+    so it does less work than the grouped kernels."""
+    import torch
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(0)
+    rows = [int(c) for c in counts if c > 0]
+    xs = [torch.randn(r, w.d, device=dev, dtype=torch.bfloat16, generator=g) for r in rows]
+    hs = [torch.randn(r, w.I, device=dev, dtype=torch.bfloat16, generator=g) for r in rows]
+    wgu = [[torch.randn(2 * w.I, w.d, device=dev, dtype=torch.bfloat16, generator=g)
+            for _ in rows] for _ in range(2)]
+    wdn = [[torch.randn(w.d, w.I, device=dev, dtype=torch.bfloat16, generator=g)
+            for _ in rows] for _ in range(2)]
+    F = torch.nn.functional.linear
+
+    def timed(fn):
+        for k in range(3):
+            fn(k)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for k in range(reps):
+            fn(k)
+        b.record()
+        torch.cuda.synchronize()
+        return 1e3 * a.elapsed_time(b) / reps
+
+    gu = timed(lambda k: [F(x, wt) for x, wt in zip(xs, wgu[k % 2])])
+    dn = timed(lambda k: [F(h, wt) for h, wt in zip(hs, wdn[k % 2])])
+    n = sum(rows)
+    fl_gu, fl_dn = 4.0 * n * w.d * w.I, 2.0 * n * w.d * w.I
+    out = {"gate_up_us": round(gu, 2), "down_us": round(dn, 2),
+           "gate_up_tflops": round(fl_gu / gu / 1e6, 1), "down_tflops": round(fl_dn / dn / 1e6, 1),
+           "kind": "torch.nn.functional.linear per expert (hipBLASLt), bf16"}
+    del xs, hs, wgu, wdn
+    torch.cuda.empty_cache()
+    return out
+
+
 def side_line(name: str, K: int, W: int) -> dict:
     """One half of the metric measured beside the main line: the decode
     stack's HBM fraction or the prefill gate/up's MFMA fraction."""
@@ -697,6 +743,8 @@ def main():
     if not args.no_side and args.workload not in ("llama7b_decode32", "prefill_skew16"):
         out["decode"] = side_line("llama7b_decode32", args.side_steps, 3)
         out["prefill"] = side_line("prefill_skew16", args.side_steps, 3)
+    if args.library_gemm and w.dtype == "bf16" and w.layers == 1 and w.K == 1 and not w.P:
+        out["library_gemm"] = library_gemm(w, counts)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
     print(json.dumps(out), flush=True)
