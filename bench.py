@@ -359,11 +359,11 @@ TRAFFIC = {
     # dominant call: the gate/up GEMM (profiles/traffic_gate_up_wide_requests.md), or
     # the whole 32-layer stack (profiles/traffic_stack_llama7b_decode32.md)
     "wide_requests": (_GEMM_SOURCES,
-                      "ddec437c0077649ec40cc55b08109983f4f3da5364293d942b91b471a132ab4c",
-                      2390474612, 58720256),
+                      "24af4288d0d3133d98cc9ccd6b32990cc6696c4197e0284a9417b4db5cbdda63",
+                      2389143341, 58720256),
     "llama7b_decode32": (_STACK_SOURCES,
-                         "82194f173573adb9f1ed7ec71ffb323ab519ff6164d8a95cb4a4e0b657dbe1d7",
-                         7873825371, 56098816),
+                         "bbd01ad3d1c5f5883598c13e3fb25edf17c7fbfd485d25e21c21ece1b2a91d4c",
+                         7873841889, 56098816),
 }
 
 
