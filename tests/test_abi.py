@@ -223,3 +223,36 @@ def test_weighted_top1_argument_errors(lib):
     assert u(1, 16, 64, FAKE, FAKE, None, FAKE, None) == 1         # no scale
     assert u(1, 16, 64, ctypes.c_void_p(4104), FAKE, FAKE, FAKE, None) == 1  # misaligned
     assert u(1, 0, 64, None, None, None, None, None) == 0
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    """With libreadme.so absent the binding raises instead of falling back to
+    any other implementation (run in a child so this process keeps its
+    loaded library)."""
+    import subprocess
+    import sys
+    code = (
+        "from paper_2410_19123_amd import _lib\n"
+        f"_lib.LIB_PATH = {str(tmp_path / 'libreadme.so')!r}\n"
+        "try:\n"
+        "    _lib.readme_padded_intermediate(100)\n"
+        "except ImportError as e:\n"
+        "    print('ImportError', e)\n"
+        "else:\n"
+        "    print('no error')\n")
+    out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True,
+                         text=True, timeout=120)
+    assert out.stdout.startswith("ImportError"), out.stdout + out.stderr
+
+
+def test_product_path_does_not_reach_the_oracle():
+    """The package and the binding never import, load or run anything under
+    oracle/ (only tests, the smoke check and the bench's CPU baseline do)."""
+    pkg = os.path.join(ROOT, "paper_2410_19123_amd")
+    # an import of the oracle package, its shared library, or a path into it
+    pat = re.compile(r"^\s*(from|import)\s+oracle\b|liboracle|[\"']oracle[\"'/]", re.M)
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".hpp", ".cpp", ".h")):
+                src = open(os.path.join(dirpath, f)).read()
+                assert not pat.search(src), os.path.join(dirpath, f)
