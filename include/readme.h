@@ -171,7 +171,13 @@ int64_t readme_padded_intermediate(int64_t I);
  *   weights streamed straight into registers (bf16; fp32 runs tile 6):
  *     12 = 128x256, 13 = 64x256, 14 = 32x256, 15 = 32x128 (deep pipeline),
  *     16 = 256x256, 19 = 128x256 (5 stages), 20 = 128x256 (6 stages),
- *     21 = 192x256 (3 stages), 22 = 192x256 (2 stages), 23 = 32x64
+ *     21 = 192x256 (3 stages), 22 = 192x256 (2 stages), 23 = 32x64,
+ *     27, 28, 29 = 32x128 of four single-group waves (6, 8, 4 stages)
+ *   several tile heights in one launch (bf16; fp32 runs tile 6), each
+ *   expert in full tiles of the first height, its remainder in the
+ *   shortest that holds it, 256 columns:
+ *     24 = 256/128/64/32, 25 = 192/128/64/32, 26 = 128/64/32 (four waves),
+ *     30 = 256/128/64, 31 = 192/128/64 (eight waves, two per SIMD)
  *   (rows of tokens x columns of outputs)
  * Results do not depend on the tile beyond fp32 summation order.  Returns
  * README_ERR_ARG for any other value.  readme_get_gemm_tile returns the

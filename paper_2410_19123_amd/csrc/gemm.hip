@@ -48,7 +48,11 @@ static int tile_by_shape(bool f32, bool gate_up, const GemmArgs& g) {
         return TILE_BD_32x128_W4;
     }
     if (gate_up) {
-        if (per_expert >= 768) return TILE_MIX_256;
+        // From 768 rows per expert: eight-wave tiles, two waves per SIMD, so
+        // one wave's LDS waits and barrier are covered by the other's MFMAs
+        // (skewed prefill 237 -> 223 us at 256 rows; request batch at d =
+        // 8192 945 -> 905 us at 192 rows, where 256 rows gave 938).
+        if (per_expert >= 768) return g.K >= 8192 ? TILE_MIX8_192 : TILE_MIX8_256;
         // 128-row tiles while their estimated count (half a tile of padding
         // per row group) fits one round on the chip's 256 CUs, so that every
         // CU streams; past that the mixed 256-row launch wins (permanent-
@@ -58,11 +62,11 @@ static int tile_by_shape(bool f32, bool gate_up, const GemmArgs& g) {
         const int64_t est = (rows / 128 + groups / 2) * ceil_div(g.N, 256);
         return est > 256 ? TILE_MIX_256 : TILE_BD_128x256;
     }
-    // Down: 192-row register-streamed tiles.  From 768 rows per expert one
-    // height (interleaved same-box runs: request batch 505 vs 510 us mixed,
-    // skewed prefill 172 vs 176 us); below, the remainders in shorter tiles
-    // (default layer 46.5 -> 44.6 us).
-    return per_expert >= 768 ? TILE_BD_192x256_S2 : TILE_MIX_192;
+    // Down: from 768 rows per expert the eight-wave mixed launch (skewed
+    // prefill, K = 704: 173 -> 146 us; request batch unchanged at 488-492
+    // us); below, four-wave 192-row tiles with the remainders in shorter
+    // tiles (default layer 46.5 -> 44.6 us against one height).
+    return per_expert >= 768 ? TILE_MIX8_256 : TILE_MIX_192;
 }
 
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s) {
@@ -73,7 +77,7 @@ hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s) {
     if (g.K >= (int64_t)32 << 16) return hipErrorInvalidValue;
     if (g.k_segs > 1 && epi != EPI_STORE) return hipErrorInvalidValue;  // segments: down only
     const int tile = tile_by_shape(f32, epi == EPI_GATE_UP_SILU, g);
-    if (!f32 && tile >= TILE_MIX_256 && tile <= TILE_MIX_128) {
+    if (!f32 && is_mix_tile(tile)) {
         if (epi == EPI_GATE_UP_SILU) return launch_mix_bf16_gate_up(tile, g, s);
         if (epi == EPI_RESID_ADD) return launch_mix_bf16_resid(tile, g, s);
         return launch_mix_bf16_store(tile, g, s);

@@ -412,12 +412,20 @@ struct Epilogue {
 // wave 2n, the up columns in wave 2n+1, so the pair meets in LDS.  The
 // waves put their fp32 sums into a row-major LDS tile, then all threads form
 // h = silu(g) * u for 8 neurons at a time and store whole output rows with
-// 16-byte stores (same fp32 arithmetic as Epilogue, so the same bits).
+// 16-byte stores (same fp32 arithmetic as Epilogue, so the same bits).  A
+// tall tile of many waves goes through LDS CH 32-row blocks at a time.
 template <int TM, int NW>
 struct EpiloguePairWaves {
     using OT = uint16_t;
     static constexpr int LDF = NW * 32 + 4;                  // fp32 row pitch
-    static constexpr int LDS_BYTES = TM * 32 * LDF * 4;
+    // 32-row blocks staged at once: the most (dividing TM) that fit 72 KB.
+    static constexpr int chunk() {
+        int c = TM;
+        while (c > 1 && (TM % c != 0 || c * 32 * LDF * 4 > 73728)) --c;
+        return c;
+    }
+    static constexpr int CH = chunk();
+    static constexpr int LDS_BYTES = CH * 32 * LDF * 4;
     static constexpr int PER_ROW = NW * 2;                   // 8-neuron pieces per row
     static_assert(NW % 2 == 0, "gate and up waves come in pairs");
 
@@ -427,35 +435,40 @@ struct EpiloguePairWaves {
         (void)wm;
         float* L = reinterpret_cast<float*>(lds_raw);
         const int lane = tid & 63;
-        __syncthreads();  // LDS free (K loop done)
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int lr = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                L[lr * LDF + wn * 32 + (lane & 31)] = acc[i][0][r];
-            }
-        __syncthreads();
         const int64_t oc0 = n0 / 2, n_out = g.N / 2;
-        for (int u = tid; u < TM * 32 * PER_ROW; u += nthreads) {
-            const int rt = u / PER_ROW, pc = u - rt * PER_ROW;
-            if (rt >= rows) continue;
-            const int64_t col = oc0 + (int64_t)pc * 8;
-            if (col >= n_out) continue;
-            const int64_t grow = g.c_rows ? (int64_t)crow[rt] : m0 + rt;
-            if (grow < 0 || grow >= g.T) continue;
-            const int ng = pc / 4, w0 = (pc % 4) * 8;    // neuron group, first neuron in it
-            const float* gt = L + rt * LDF + (2 * ng) * 32 + w0;
-            const float* up = L + rt * LDF + (2 * ng + 1) * 32 + w0;
-            uint32_t packed[4];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const uint32_t lo = f32_to_bf16(silu_f32(gt[2 * k]) * up[2 * k]);
-                const uint32_t hi = f32_to_bf16(silu_f32(gt[2 * k + 1]) * up[2 * k + 1]);
-                packed[k] = lo | (hi << 16);
+        for (int c0 = 0; c0 < TM; c0 += CH) {
+            __syncthreads();  // LDS free (K loop or the previous block done)
+#pragma unroll
+            for (int i = 0; i < CH; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int lr = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                    L[lr * LDF + wn * 32 + (lane & 31)] = acc[c0 + i][0][r];
+                }
+            __syncthreads();
+            for (int u = tid; u < CH * 32 * PER_ROW; u += nthreads) {
+                const int rl = u / PER_ROW, pc = u - rl * PER_ROW;  // row in the block
+                const int rt = c0 * 32 + rl;                        // row in the tile
+                if (rt >= rows) continue;
+                const int64_t col = oc0 + (int64_t)pc * 8;
+                if (col >= n_out) continue;
+                const int64_t grow = g.c_rows ? (int64_t)crow[rt] : m0 + rt;
+                if (grow < 0 || grow >= g.T) continue;
+                const int ng = pc / 4, w0 = (pc % 4) * 8;  // neuron group, first neuron in it
+                const float* gt = L + rl * LDF + (2 * ng) * 32 + w0;
+                const float* up = L + rl * LDF + (2 * ng + 1) * 32 + w0;
+                uint32_t packed[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const uint32_t lo = f32_to_bf16(silu_f32(gt[2 * k]) * up[2 * k]);
+                    const uint32_t hi = f32_to_bf16(silu_f32(gt[2 * k + 1]) * up[2 * k + 1]);
+                    packed[k] = lo | (hi << 16);
+                }
+                const u32x4 v = {packed[0], packed[1], packed[2], packed[3]};
+                *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(g.C) + grow * g.ldc + col) =
+                    v;
             }
-            const u32x4 v = {packed[0], packed[1], packed[2], packed[3]};
-            *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(g.C) + grow * g.ldc + col) = v;
         }
     }
 };
@@ -929,7 +942,12 @@ enum TileCfg {
     TILE_BD_32x128_W4 = 27,     // 6 K-steps in flight
     TILE_BD_32x128_W4_S8 = 28,  // 8 K-steps in flight
     TILE_BD_32x128_W4_S4 = 29,  // 4 K-steps in flight
-    TILE_LAST = TILE_BD_32x128_W4_S4,
+    // Tiles of several heights in one launch, eight waves (two per SIMD) of
+    // one 32-column weight group each (256 columns; gate/up paired across
+    // waves):
+    TILE_MIX8_256 = 30,  // 256 (2 K-steps), 128, 64 rows (4 K-steps)
+    TILE_MIX8_192 = 31,  // 192 (3 K-steps), 128, 64 rows (4 K-steps)
+    TILE_LAST = TILE_MIX8_192,
 };
 
 // Launches one tile configuration (instantiated per element type and

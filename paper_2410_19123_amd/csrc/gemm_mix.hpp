@@ -6,9 +6,10 @@
 // each row group (expert) is cut into full tiles of the largest height B0,
 // and its remainder r goes to the class of the smallest height that holds
 // it (B1 >= r > B2 -> class 1, and so on); a remainder above B1 takes one
-// more B0 tile.  All classes are register-streamed tiles of four waves and
-// 256 output columns (BdTile), so the launch runs one kernel whose
-// workgroups pick their class's tile routine.
+// more B0 tile.  All classes are register-streamed tiles (BdTile) of 256
+// output columns with the same waves -- four waves of two 32-column groups,
+// or eight waves (two per SIMD) of one group each -- so the launch runs one
+// kernel whose workgroups pick their class's tile routine.
 //
 // Order.  The blocks of class 0 come first, then class 1, and so on, so the
 // dispatcher starts the longest tiles first and fills the tail of the launch
@@ -120,22 +121,29 @@ __device__ __forceinline__ bool mix_locate(const GemmArgs& g, int c, int L, Tile
     return false;
 }
 
-template <int B0, int B1, int B2, int B3, int S0, int S1, int S2, int S3, int EPI>
+// NW waves of TN 32-column groups each (NW * TN = 8: 256 columns).
+template <int B0, int B1, int B2, int B3, int S0, int S1, int S2, int S3, int EPI, int NW,
+          int TN>
 struct MixKernel {
+    static_assert(NW * TN == 8, "256 output columns per tile");
     using Mix = MixRows<B0, B1, B2, B3>;
     // Classes that are absent reuse class 0's routine type (never run).
-    using T0 = BdTile<B0, 4, 2, S0, false, EPI>;
-    using T1 = BdTile<(B1 > 0 ? B1 : B0), 4, 2, (B1 > 0 ? S1 : S0), false, EPI>;
-    using T2 = BdTile<(B2 > 0 ? B2 : B0), 4, 2, (B2 > 0 ? S2 : S0), false, EPI>;
-    using T3 = BdTile<(B3 > 0 ? B3 : B0), 4, 2, (B3 > 0 ? S3 : S0), false, EPI>;
+    using T0 = BdTile<B0, NW, TN, S0, false, EPI>;
+    using T1 = BdTile<(B1 > 0 ? B1 : B0), NW, TN, (B1 > 0 ? S1 : S0), false, EPI>;
+    using T2 = BdTile<(B2 > 0 ? B2 : B0), NW, TN, (B2 > 0 ? S2 : S0), false, EPI>;
+    using T3 = BdTile<(B3 > 0 ? B3 : B0), NW, TN, (B3 > 0 ? S3 : S0), false, EPI>;
     static constexpr int cmax(int a, int b) { return a > b ? a : b; }
     static constexpr int SLOTS =
         cmax(cmax(T0::LDS_SLOTS, T1::LDS_SLOTS), cmax(T2::LDS_SLOTS, T3::LDS_SLOTS));
 };
 
-template <int B0, int B1, int B2, int B3, int S0, int S1, int S2, int S3, int EPI>
-__global__ __launch_bounds__(256) void k_grouped_gemm_mix(GemmArgs g) {
-    using K = MixKernel<B0, B1, B2, B3, S0, S1, S2, S3, EPI>;
+// Eight-wave tiles are compiled for two waves per SIMD (at most 256
+// registers per lane, accumulators included).
+template <int B0, int B1, int B2, int B3, int S0, int S1, int S2, int S3, int EPI, int NW,
+          int TN>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(NW > 4 ? 2 : 1)))
+void k_grouped_gemm_mix(GemmArgs g) {
+    using K = MixKernel<B0, B1, B2, B3, S0, S1, S2, S3, EPI, NW, TN>;
     using Mix = typename K::Mix;
     __shared__ u32x4 lds[K::SLOTS];
     __shared__ int32_t crow[B0];
@@ -162,10 +170,11 @@ __global__ __launch_bounds__(256) void k_grouped_gemm_mix(GemmArgs g) {
 }
 
 // Host: block ranges per class from upper bounds of their tile counts.
-template <int B0, int B1, int B2, int B3, int S0, int S1, int S2, int S3, int EPI>
+template <int B0, int B1, int B2, int B3, int S0, int S1, int S2, int S3, int EPI, int NW,
+          int TN>
 inline hipError_t launch_mix(GemmArgs g, hipStream_t s) {
     using Mix = MixRows<B0, B1, B2, B3>;
-    g.n_tiles = (int)ceil_div(g.N, 256);
+    g.n_tiles = (int)ceil_div(g.N, NW * TN * 32);
     const int64_t groups = (int64_t)g.E + g.shared_groups;
     int64_t start = 0;
     for (int c = 0; c < 4; ++c) {
@@ -185,19 +194,28 @@ inline hipError_t launch_mix(GemmArgs g, hipStream_t s) {
     g.mix_start[4] = (int)start;
     if (start == 0) return hipSuccess;
     if (start > 0x7fffffffLL) return hipErrorInvalidValue;
-    k_grouped_gemm_mix<B0, B1, B2, B3, S0, S1, S2, S3, EPI>
-        <<<dim3((unsigned)start), dim3(256), 0, s>>>(g);
+    k_grouped_gemm_mix<B0, B1, B2, B3, S0, S1, S2, S3, EPI, NW, TN>
+        <<<dim3((unsigned)start), dim3(NW * 64), 0, s>>>(g);
     return hipGetLastError();
 }
 
 template <int EPI>
 hipError_t launch_mix_tile(int tile, GemmArgs g, hipStream_t s) {
     switch (tile) {
-        case TILE_MIX_256: return launch_mix<256, 128, 64, 32, 2, 4, 4, 4, EPI>(g, s);
-        case TILE_MIX_192: return launch_mix<192, 128, 64, 32, 2, 4, 4, 4, EPI>(g, s);
-        case TILE_MIX_128: return launch_mix<128, 64, 32, 0, 4, 4, 4, 4, EPI>(g, s);
+        case TILE_MIX_256: return launch_mix<256, 128, 64, 32, 2, 4, 4, 4, EPI, 4, 2>(g, s);
+        case TILE_MIX_192: return launch_mix<192, 128, 64, 32, 2, 4, 4, 4, EPI, 4, 2>(g, s);
+        case TILE_MIX_128: return launch_mix<128, 64, 32, 0, 4, 4, 4, 4, EPI, 4, 2>(g, s);
+        // Eight waves: a 32-row class would give a wave less than one
+        // 8-row activation load, so remainders of up to 64 rows take 64.
+        case TILE_MIX8_256: return launch_mix<256, 128, 64, 0, 2, 4, 4, 4, EPI, 8, 1>(g, s);
+        case TILE_MIX8_192: return launch_mix<192, 128, 64, 0, 3, 4, 4, 4, EPI, 8, 1>(g, s);
         default: return hipErrorInvalidValue;
     }
+}
+
+inline bool is_mix_tile(int tile) {
+    return (tile >= TILE_MIX_256 && tile <= TILE_MIX_128) || tile == TILE_MIX8_256 ||
+           tile == TILE_MIX8_192;
 }
 
 hipError_t launch_mix_bf16_gate_up(int tile, GemmArgs g, hipStream_t s);

@@ -185,7 +185,7 @@ def test_streamed_buffers_checked_before_any_launch(lib):
 
 def test_tile_override_is_per_thread(lib):
     import threading
-    assert lib.readme_set_gemm_tile(30) == 1
+    assert lib.readme_set_gemm_tile(32) == 1
     assert lib.readme_set_gemm_tile(-1) == 1
     assert lib.readme_set_gemm_tile(5) == 0
     seen = []

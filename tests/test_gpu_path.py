@@ -345,8 +345,36 @@ def test_stack_layer_norm_widths(L, oracle_mod, d):
     U.close(delta, oracle_mod.layer(x_in, offsets, *host, eps=1e-5), f"d {d}")
 
 
+@pytest.mark.parametrize("tile", [0, 12, 22, 24, 25, 26, 27, 30, 31])
+def test_stack_tiles_match_oracle(L, oracle_mod, tile):
+    """Two stacked layers (pre-norm, expert FFN, residual added in the down
+    projection's epilogue) with one forced tile, on ragged blocks that put
+    rows in every height class of the mixed launches; 16 K-steps in the
+    gate/up GEMM."""
+    _say("stack tile", tile)
+    counts = np.array([300, 0, 97, 31, 513], np.int32)
+    w = wl.Workload("t", T=int(counts.sum()), d=1024, E=5, I=320, dtype="bf16", layers=2)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    host = [wl.make_experts(w, 90 + tile, layer=l) for l in range(w.layers)]
+    packed = [L.readme_pack_experts(*U.weights_to_dev(*h)) for h in host]
+    x0 = wl.bf16_bits_to_f32(wl.make_x(w, 90 + tile)).astype(np.float32)
+    xr = U.to_dev(x0)
+    L.readme_set_gemm_tile(tile)
+    try:
+        L.readme_moe_ffn_stack(xr, U.to_dev(offsets), packed, w.E, w.I)
+        torch.cuda.synchronize()
+    finally:
+        L.readme_set_gemm_tile(0)
+    got = U.from_dev(xr).astype(np.float64)
+    ref = x0.copy()
+    for l in range(w.layers):
+        ref = (ref.astype(np.float64) + oracle_mod.layer(ref, offsets, *host[l], eps=1e-5))
+        ref = ref.astype(np.float32)
+    U.close(got - x0, ref.astype(np.float64) - x0, f"stack tile {tile}")
+
+
 # ------------------------------------------------------ every tile config
-@pytest.mark.parametrize("tile", list(range(1, 30)))
+@pytest.mark.parametrize("tile", list(range(1, 32)))
 def test_every_gemm_tile_matches_oracle(L, oracle_mod, tile):
     """Each workgroup tile of the grouped GEMM, on ragged blocks (empty,
     single-row, tile +- 1 and multi-tile experts) in bf16 and fp32."""

@@ -32,7 +32,7 @@ def _pack(L, w, seed):
         *U.weights_to_dev(*wl.make_permanent(w, seed)))
 
 
-@pytest.mark.parametrize("tile", list(range(0, 24)))
+@pytest.mark.parametrize("tile", list(range(0, 32)))
 def test_every_tile_with_permanent_expert(L, oracle_mod, tile):
     """Each GEMM tile configuration: the permanent slices as extra row
     groups over every routed row (gate/up) and as extra K segments (down),

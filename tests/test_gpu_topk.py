@@ -90,7 +90,7 @@ def test_topk_layer_full_workload(L, oracle_mod):
     U.close(got["y"], ref["y"], w.name)
 
 
-@pytest.mark.parametrize("tile", [0, 1, 6, 12, 15, 17, 21])
+@pytest.mark.parametrize("tile", [0, 1, 6, 12, 15, 17, 21, 24, 27, 30, 31])
 def test_topk_layer_tiles(L, oracle_mod, tile):
     """All rows of a small ragged top-3 layer, through the LDS-staged and the
     register-streamed GEMM kernels (the pair -> token gather in each)."""
