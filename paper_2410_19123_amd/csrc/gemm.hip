@@ -62,11 +62,11 @@ static int tile_by_shape(bool f32, bool gate_up, const GemmArgs& g) {
         const int64_t est = (rows / 128 + groups / 2) * ceil_div(g.N, 256);
         return est > 256 ? TILE_MIX_256 : TILE_BD_128x256;
     }
-    // Down: from 768 rows per expert the eight-wave mixed launch (skewed
-    // prefill, K = 704: 173 -> 146 us; request batch unchanged at 488-492
-    // us); below, four-wave 192-row tiles with the remainders in shorter
-    // tiles (default layer 46.5 -> 44.6 us against one height).
-    return per_expert >= 768 ? TILE_MIX8_256 : TILE_MIX_192;
+    // Down: eight-wave mixed launches, 256-row tiles from 768 rows per
+    // expert (skewed prefill, K = 704: 173 -> 146 us against four-wave
+    // 192-row tiles; request batch 493 -> 486 us), 192-row tiles below
+    // (default layer 45.4 -> 41.3 us against the four-wave mixed launch).
+    return per_expert >= 768 ? TILE_MIX8_256 : TILE_MIX8_192;
 }
 
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s) {
