@@ -359,11 +359,11 @@ TRAFFIC = {
     # dominant call: the gate/up GEMM (profiles/traffic_gate_up_wide_requests.md), or
     # the whole 32-layer stack (profiles/traffic_stack_llama7b_decode32.md)
     "wide_requests": (_GEMM_SOURCES,
-                      "24af4288d0d3133d98cc9ccd6b32990cc6696c4197e0284a9417b4db5cbdda63",
-                      2389143341, 58720256),
+                      "368abb4ad61a1332bbdbfda26b60e67e6948ae68ae2e6beeff00c2a26a9f25e9",
+                      2258390854, 58720256),
     "llama7b_decode32": (_STACK_SOURCES,
-                         "bbd01ad3d1c5f5883598c13e3fb25edf17c7fbfd485d25e21c21ece1b2a91d4c",
-                         7873841889, 56098816),
+                         "c05bf8d9a36f74b370ab6ad0b6a55c578aedfd525619e5a699fc61640e1c25af",
+                         7873845757, 56098816),
 }
 
 
