@@ -53,14 +53,16 @@ static int tile_by_shape(bool f32, bool gate_up, const GemmArgs& g) {
         // (skewed prefill 237 -> 223 us at 256 rows; request batch at d =
         // 8192 945 -> 905 us at 192 rows, where 256 rows gave 938).
         if (per_expert >= 768) return g.K >= 8192 ? TILE_MIX8_192 : TILE_MIX8_256;
-        // 128-row tiles while their estimated count (half a tile of padding
-        // per row group) fits one round on the chip's 256 CUs, so that every
-        // CU streams; past that the mixed 256-row launch wins (permanent-
-        // expert groups: 401 estimated tiles, 142 -> 123 us).
+        // 128-row tiles of four waves while their estimated count (half a
+        // tile of padding per row group) fits one round on the chip's 256
+        // CUs, so that every CU streams (eight waves: 74-76 vs 71 us at the
+        // Llama-7B-shaped layer); past that the eight-wave mixed 256-row
+        // launch (permanent-expert groups, 401 estimated tiles: 129 -> 120
+        // us against the four-wave mixed launch; top-2 pairs: 127 -> 117 us).
         const int64_t groups = g.E + g.shared_groups;
         const int64_t rows = g.T * (1 + g.shared_groups);
         const int64_t est = (rows / 128 + groups / 2) * ceil_div(g.N, 256);
-        return est > 256 ? TILE_MIX_256 : TILE_BD_128x256;
+        return est > 256 ? TILE_MIX8_256 : TILE_BD_128x256;
     }
     // Down: eight-wave mixed launches, 256-row tiles from 768 rows per
     // expert (skewed prefill, K = 704: 173 -> 146 us against four-wave
