@@ -146,16 +146,6 @@ struct TileLoc {
     int mt_base;      // M tiles of size BMG (locate_tile) of experts before e
 };
 
-// Inclusive prefix sum over the 64 lanes of a wave.
-__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const int u = __shfl_up(v, off, 64);
-        if (lane >= off) v += u;
-    }
-    return v;
-}
-
 // Rows [s, en) of row group ee, offsets clamped to [0, T] (a corrupt offsets
 // array cannot make a tile leave the rows); returns its M tiles of size BM.
 // Groups 0 .. E-1 are the experts; a permanent-expert group (ee >= E) covers

@@ -109,7 +109,12 @@ def _ids_case(kind, T, E, seed):
     # many 1024-id rounds with many experts, invalid ids among 200 experts,
     # and sizes on both sides of 16 rounds
     ("uniform", 16384, 256), ("invalid", 9000, 200), ("local", 16384, 8),
-    ("uniform", 16385, 8), ("empty_ends", 16383, 64)])
+    ("uniform", 16385, 8), ("empty_ends", 16383, 64),
+    # the many-workgroup sort (8192 <= T <= 2^20) at its edges: one expert at
+    # the threshold, one token below it, the largest size with 256 experts,
+    # and one token past it (back on one workgroup) with invalid ids
+    ("one_expert", 8192, 1), ("uniform", 8191, 8), ("uniform", 1 << 20, 256),
+    ("invalid", (1 << 20) + 1, 16)])
 def test_group_bit_exact(L, oracle_mod, kind, T, E):
     _say("group", kind, T, E)
     ids = _ids_case(kind, T, E, seed=T + E)
