@@ -359,11 +359,11 @@ TRAFFIC = {
     # dominant call: the gate/up GEMM (profiles/traffic_gate_up_wide_requests.md), or
     # the whole 32-layer stack (profiles/traffic_stack_llama7b_decode32.md)
     "wide_requests": (_GEMM_SOURCES,
-                      "368abb4ad61a1332bbdbfda26b60e67e6948ae68ae2e6beeff00c2a26a9f25e9",
-                      2258390854, 58720256),
+                      "0cc427167486bee7185255d8e322f5384fe1bfe068a2a566d4a5858ae9876630",
+                      2258144601, 58720256),
     "llama7b_decode32": (_STACK_SOURCES,
-                         "c05bf8d9a36f74b370ab6ad0b6a55c578aedfd525619e5a699fc61640e1c25af",
-                         7873845757, 56098816),
+                         "26f7af67022fd5e0b981bb9f4e5fa4610fcbb556c73d6b2899ab440b1faa3039",
+                         7873843072, 56098816),
 }
 
 
