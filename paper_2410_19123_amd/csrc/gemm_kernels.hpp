@@ -259,16 +259,21 @@ __device__ __forceinline__ GemmArgs tile_args(const GemmArgs& g, int e) {
 // group, fragment, lane) is the same in every K segment; the segment's base
 // and the step within it are wave-uniform.  Segment 0 is the tile's own
 // weights (index e), segment s >= 1 the permanent slice of index E+s-1.
+//
+// The packed layout (pack.hip) stores each index's matrix as 4 KB blocks of
+// 32 rows x 128 bytes of K, ordered (K block, row group): K block kt of row
+// group grp is at at(kt) + grp * 4096, with at(kt) = base + kt * step_bytes
+// and step_bytes = (N / 32) * 4096.
 struct WeightSteps {
     const char* own;     // index e
     const char* B0;      // index 0
     int64_t estride;     // bytes per weight index
-    int64_t step_bytes;  // bytes per K-step of one row group
-    uint32_t nks;        // K-steps per segment
+    int64_t step_bytes;  // bytes per 128-byte K block (all row groups of it)
+    uint32_t nks;        // K blocks per segment
     uint32_t mult;       // ceil(2^32 / nks) with several segments, else 0
     int E;
 
-    // Segment of K-step kt = floor(kt * mult / 2^32), exact for kt and nks
+    // Segment of K block kt = floor(kt * mult / 2^32), exact for kt and nks
     // below 2^16 (the launcher checks K); 0 throughout with one segment.
     __device__ __forceinline__ const char* at(int kt) const {
         const uint32_t sg = __umulhi((uint32_t)kt, mult);
@@ -280,16 +285,15 @@ struct WeightSteps {
 // SEG: the kernel may run K segments (the down projection of a layer with a
 // permanent expert); otherwise the segment is 0 at compile time.
 template <bool SEG>
-__device__ __forceinline__ WeightSteps weight_steps(const GemmArgs& g, int e, int esz,
-                                                    int64_t bk, int64_t step_bytes) {
+__device__ __forceinline__ WeightSteps weight_steps(const GemmArgs& g, int e, int esz) {
     WeightSteps w;
     const int segs = SEG && g.k_segs > 1 ? g.k_segs : 1;
     w.B0 = reinterpret_cast<const char*>(g.B);
     w.estride = g.b_expert_stride * esz;
     const int we = g.b_index && e < g.E ? g.b_index[e] : e;  // slot of expert e, if cached
     w.own = w.B0 + (int64_t)we * w.estride;
-    w.step_bytes = step_bytes;
-    w.nks = (uint32_t)(g.K / segs / bk);
+    w.step_bytes = (g.N >> 5) * 4096;
+    w.nks = (uint32_t)(g.K * esz / segs / 128);
     w.mult = segs > 1 ? (uint32_t)(((1ull << 32) + w.nks - 1) / w.nks) : 0u;
     w.E = g.E;
     return w;
@@ -528,13 +532,12 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs args) {
         }
         a_src[i] = Ab + row * g.lda * ESZ + swzk(lane % KC, r) * 16;
     }
-    // B sources.  A 32-row group's packed weights form one contiguous stream
-    // along K (4 KB per 128-byte K-step), so a step of the tile copies
-    // KC/2 KB of each group's stream: KB q of the stage's B region is KB
-    // q % (KC/2) of group q / (KC/2).  N tiles past the last group reuse it
-    // (their columns are never stored).
-    const WeightSteps wst = weight_steps<EPI == EPI_STORE>(g, e, ESZ, BK, KC * 512);
-    const int64_t group_bytes = (int64_t)wst.nks * KC * 512;  // per K segment
+    // B sources.  A 32-row group's packed weights are 4 KB per 128-byte K
+    // block, so a step of the tile copies KC/2 KB of each group's block:
+    // KB q of the stage's B region is KB q % (KC/2) of group q / (KC/2)
+    // (with half-size steps, of the block's first or second half).  N tiles
+    // past the last group reuse it (their columns are never stored).
+    const WeightSteps wst = weight_steps<EPI == EPI_STORE>(g, e, ESZ);
     uint32_t b_off[B_INS];
 #pragma unroll
     for (int i = 0; i < B_INS; ++i) {
@@ -542,13 +545,13 @@ __global__ __launch_bounds__(WGM* WGN * 64) void k_grouped_gemm(GemmArgs args) {
         int64_t grp = (n0 >> 5) + q / (KC / 2);
         const int64_t last = (g.N >> 5) - 1;
         grp = grp < last ? grp : last;
-        b_off[i] = (uint32_t)(grp * group_bytes + (q % (KC / 2)) * 1024 + lane * 16);
+        b_off[i] = (uint32_t)(grp * 4096 + (q % (KC / 2)) * 1024 + lane * 16);
     }
 
     auto issue = [&](int stage, int kt) {
         u32x4* base = lds + stage * STAGE;
         const int64_t aoff = (int64_t)kt * KC * 16;
-        const char* bs = wst.at(kt);
+        const char* bs = KC == 8 ? wst.at(kt) : wst.at(kt >> 1) + (kt & 1) * 2048;
 #pragma unroll
         for (int i = 0; i < A_INS; ++i) dma16(a_src[i] + aoff, base + (wave + NW * i) * 64);
 #pragma unroll
@@ -699,14 +702,14 @@ struct BdTile {
     // Weight fragments of this wave: row group (col0/32 + j), clamped to the
     // last group for columns past N (loaded, never stored).
     const int nk = (int)(g.K / BK);
-    const WeightSteps wst = weight_steps<EPI == EPI_STORE>(g, t.e, ESZ, BK, 4096);
+    const WeightSteps wst = weight_steps<EPI == EPI_STORE>(g, t.e, ESZ);
     uint32_t b_off[TN];
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
         int64_t grp = (col0 >> 5) + j;
         const int64_t last = (g.N >> 5) - 1;
         grp = grp < last ? grp : last;
-        b_off[j] = (uint32_t)(grp * wst.nks * 4096 + lane * 16);
+        b_off[j] = (uint32_t)(grp * 4096 + lane * 16);
     }
 
     u32x4 bq[S][TN][CPR / 2];
