@@ -359,11 +359,11 @@ TRAFFIC = {
     # dominant call: the gate/up GEMM (profiles/traffic_gate_up_wide_requests.md), or
     # the whole 32-layer stack (profiles/traffic_stack_llama7b_decode32.md)
     "wide_requests": (_GEMM_SOURCES,
-                      "0cc427167486bee7185255d8e322f5384fe1bfe068a2a566d4a5858ae9876630",
-                      2258144601, 58720256),
+                      "d4951901d248354cb44ddbec258d61f67ce545529dedb524aa5105a139737687",
+                      2257194574, 58720256),
     "llama7b_decode32": (_STACK_SOURCES,
-                         "26f7af67022fd5e0b981bb9f4e5fa4610fcbb556c73d6b2899ab440b1faa3039",
-                         7873843072, 56098816),
+                         "be1919bf82f2577568b294126229d686c2514bd08643daebe94322fb15a5c4cd",
+                         7874061121, 56098816),
 }
 
 
