@@ -356,11 +356,15 @@ _STACK_SOURCES = ["csrc/gemm_kernels.hpp", "csrc/gemm.hip", "csrc/gemm_bf16_gate
                   "csrc/common.hpp", "csrc/internal.hpp", "csrc/pack.hip", "workloads.py"]
 TRAFFIC = {
     # workload: (sources, their sha256, read bytes, written bytes) per launch of the
-    # dominant call: the gate/up GEMM (profiles/traffic_gate_up_wide_requests.md), or
-    # the whole 32-layer stack (profiles/traffic_stack_llama7b_decode32.md)
+    # dominant call: the gate/up GEMM (profiles/traffic_gate_up_wide_requests.md,
+    # profiles/traffic_gate_up_prefill_skew16.md), or the whole 32-layer stack
+    # (profiles/traffic_stack_llama7b_decode32.md)
     "wide_requests": (_GEMM_SOURCES,
                       "d4951901d248354cb44ddbec258d61f67ce545529dedb524aa5105a139737687",
                       2257194574, 58720256),
+    "prefill_skew16": (_GEMM_SOURCES,
+                       "d4951901d248354cb44ddbec258d61f67ce545529dedb524aa5105a139737687",
+                       609878110, 23068672),
     "llama7b_decode32": (_STACK_SOURCES,
                          "be1919bf82f2577568b294126229d686c2514bd08643daebe94322fb15a5c4cd",
                          7874061121, 56098816),
