@@ -73,3 +73,27 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_traffic_entries_follow_their_sources(tmp_path, monkeypatch):
+    """A calibrated traffic entry gives its read + written bytes only for
+    the exact sources it was taken with, and null as soon as any of them
+    differs (a kernel changed since the counters were read)."""
+    import os
+    import shutil
+    for name, (sources, sha, rd, wr) in bench.TRAFFIC.items():
+        assert bench.traffic_bytes(name) in (None, rd + wr), name
+        assert rd > 0 and wr > 0 and len(sha) == 64
+    # a copy of the package with one source byte changed
+    pkg = os.path.join(os.path.dirname(os.path.abspath(bench.__file__)), "paper_2410_19123_amd")
+    fake = tmp_path / "paper_2410_19123_amd"
+    for rel in set(r for s, _, _, _ in bench.TRAFFIC.values() for r in s):
+        dst = fake / rel
+        dst.parent.mkdir(parents=True, exist_ok=True)
+        shutil.copyfile(os.path.join(pkg, rel), dst)
+    with open(fake / "csrc" / "gemm_kernels.hpp", "ab") as f:
+        f.write(b"\n")
+    monkeypatch.setattr(bench, "__file__", str(tmp_path / "bench.py"))
+    for name in bench.TRAFFIC:
+        assert bench.traffic_bytes(name) is None, name
+    assert bench.traffic_bytes("tiny_f32") is None   # no entry
