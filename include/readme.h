@@ -13,7 +13,9 @@
  *     F_e(x) = W_down^e ( silu(W_gate^e x) * (W_up^e x) ).
  *
  * The calls, in path order:
- *     readme_route            one top-1 expert id per token
+ *     readme_router_tf        the router G: one causal transformer block over
+ *                             each request's tokens, then the gate below
+ *     readme_route            one top-1 expert id per token (G's final gate)
  *     readme_group_by_expert  histogram, exclusive scan, stable permutation,
  *                             row gather into expert-contiguous order
  *     readme_moe_ffn          every expert's SwiGLU FFN on its token block
@@ -633,6 +635,123 @@ readme_status readme_moe_ffn_stack_counts(int64_t T, int64_t d, int32_t E, int64
                                           float *x_resid_grouped, float rms_eps,
                                           void *workspace, size_t workspace_bytes,
                                           void *stream);
+
+/*
+ * The pre-gating router G itself (Sec. 2.3, Table 1): one causal transformer
+ * block over each request's tokens, whose normed output feeds the gate of
+ * readme_route.  G reads a token and the tokens before it in the same
+ * request, and nothing of the expert layers, so it runs once per token
+ * before any layer (Sec. 2.3).  The paper fixes the block's type and sizes
+ * (one layer, four heads, width 512, SwiGLU MLP, RoPE, RMSNorm); its wiring
+ * here is the pre-norm residual block of the Llama family:
+ *   x  = emb[token]                     fp32 residual (bf16 table rows; an id
+ *                                       outside [0, V) embeds as zeros)
+ *   a  = bf16(rmsnorm(x)),  q|k|v = bf16(a [Wq; Wk; Wv]^T)
+ *   q, k <- bf16(RoPE(q, k)) (readme_rope)
+ *   o  = bf16(causal attention(q, k, v)) (readme_attention_causal)
+ *   x += o Wo^T
+ *   x += W2 (silu(W1 m) * W3 m),  m = bf16(rmsnorm(x))
+ *   f  = bf16(rmsnorm(x)),  expert_ids, logits = readme_route(f, w_router, bias)
+ * rmsnorm has no gain: r = 1 / sqrt(mean x^2 + rms_eps), fp32.  Heads are
+ * D / 128 slices of 128 dims; bf16 weights only.
+ *
+ * readme_router_tf_pack -- one-time repack of the block's weights into
+ *   `packed` (readme_router_tf_packed_bytes(D, F) bytes, device, 16-byte
+ *   aligned):  wq, wk, wv, wo [D][D]; w1, w3 [F][D]; w2 [D][F]  (bf16,
+ *   [out][in] row-major, device).  README_ERR_WORKSPACE if packed_bytes is
+ *   smaller than required.
+ *
+ * readme_router_tf -- the router over T tokens of R requests:
+ *   tokens       [T]      int32   token ids
+ *   req_offsets  [R+1]    int32   request r is tokens [req_offsets[r],
+ *                                 req_offsets[r+1]); req_offsets[0] = 0,
+ *                                 req_offsets[R] = T, non-decreasing (empty
+ *                                 requests allowed).  Other values give
+ *                                 unspecified results but no access outside
+ *                                 the arrays.
+ *   emb          [V][D]   bf16    embedding table
+ *   packed                        from readme_router_tf_pack(D, F, ...)
+ *   w_router     [E][D]   bf16,   bias [E] fp32 or NULL: the gate
+ *   expert_ids   [T]      int32 out;  logits [T][E] fp32 out or NULL
+ *   workspace    >= readme_router_tf_workspace_bytes(T, D, F) bytes
+ * On return the workspace holds every intermediate, each region at
+ * readme_router_tf_workspace_offset(T, D, F, region):
+ *   README_RTF_X     [T][D]   fp32   the block's output x (before the final norm)
+ *   README_RTF_A     [T][D]   bf16   a
+ *   README_RTF_QKV   [T][3D]  bf16   q | k | v (q and k rotated)
+ *   README_RTF_O     [T][D]   bf16   attention output
+ *   README_RTF_M     [T][D]   bf16   the MLP's normed input m
+ *   README_RTF_H     [T][Fp]  bf16   silu(W1 m) * W3 m, Fp = readme_padded_intermediate(F)
+ *   README_RTF_FEAT  [T][D]   bf16   f, the gate's input
+ *   README_RTF_POS   [T]      int32  each token's position in its request
+ *   README_RTF_OFFS  [2]      int32  {0, T}
+ * Requires D > 0 a multiple of 128 and at most 16384, F >= 1 (with
+ * 4 * Fp * D < 2^31), 1 <= E <= README_MAX_EXPERTS, V >= 1, rms_eps >= 0,
+ * R >= 1 when T > 0.  The size queries return 0 (offset: -1) for arguments
+ * outside that set.
+ */
+#define README_RTF_X 0
+#define README_RTF_A 1
+#define README_RTF_QKV 2
+#define README_RTF_O 3
+#define README_RTF_M 4
+#define README_RTF_H 5
+#define README_RTF_FEAT 6
+#define README_RTF_POS 7
+#define README_RTF_OFFS 8
+#define README_RTF_END 9 /* offset of the end = the workspace size */
+
+size_t readme_router_tf_packed_bytes(int64_t D, int64_t F);
+readme_status readme_router_tf_pack(int64_t D, int64_t F, const void *wq, const void *wk,
+                                    const void *wv, const void *wo, const void *w1,
+                                    const void *w3, const void *w2, void *packed,
+                                    size_t packed_bytes, void *stream);
+size_t readme_router_tf_workspace_bytes(int64_t T, int64_t D, int64_t F);
+int64_t readme_router_tf_workspace_offset(int64_t T, int64_t D, int64_t F, int32_t region);
+readme_status readme_router_tf(int64_t T, int32_t R, int64_t D, int64_t F, int32_t E,
+                               int64_t V, const int32_t *tokens, const int32_t *req_offsets,
+                               const void *emb, const void *packed, const void *w_router,
+                               const float *bias, float rms_eps, int32_t *expert_ids,
+                               float *logits, void *workspace, size_t workspace_bytes,
+                               void *stream);
+
+/*
+ * readme_request_positions -- pos[t] = t - req_offsets[r] for the request r
+ * holding token t (requests as in readme_router_tf): the position that
+ * RoPE rotates by and that bounds the causal attention.  pos [T] int32 out.
+ */
+readme_status readme_request_positions(int64_t T, int32_t R, const int32_t *req_offsets,
+                                       int32_t *pos, void *stream);
+
+/*
+ * readme_rope -- rotary position embedding (RoPE, the positional encoding of
+ * Table 1's block) in place on H heads of 128 bf16 values per row: row t at
+ * x + t * ld, head h at columns 128h .. 128h+127.  For i < 64 the pair
+ * (x_i, x_{i+64}) of each head turns by the angle pos[t] * 10000^(-2i/128):
+ *   x_i     <- x_i cos - x_{i+64} sin
+ *   x_{i+64} <- x_{i+64} cos + x_i sin
+ * (the rotate-half form), angle, sine, cosine and products in fp64 without
+ * fused multiply-adds, each result rounded to fp32 and then to bf16 (nearest
+ * even).  pos [T] int32 (readme_request_positions).  Requires ld >= 128 H.
+ */
+readme_status readme_rope(int64_t T, int32_t H, const int32_t *pos, void *x, int64_t ld,
+                          void *stream);
+
+/*
+ * readme_attention_causal -- multi-head attention of each token over its
+ * request's prefix (Sec. 2.3: G sees the current and earlier tokens):
+ *   o[t]_h = sum_j w_tj v[j]_h / sum_j w_tj,   w_tj = exp(q[t]_h . k[j]_h / sqrt(128) - m_t)
+ * over j = t - pos[t] .. t, per head h of 128 dims.  Scores and the running
+ * softmax in fp32; the weights enter the value product as a bf16 pair
+ * (hi + lo, about 16 significant bits), so o is the exact result up to
+ * about 2^-16 of the largest |v| plus the final bf16 rounding.
+ *   q, k, v  [T][ld_in] bf16 (head h at columns 128h ..), o [T][ld_out] bf16
+ *   out, pos [T] int32.  Requires ld_in, ld_out >= 128 H and multiples of 8,
+ *   16-byte aligned q, k, v, o, H <= 65535.  o must not overlap q, k or v.
+ */
+readme_status readme_attention_causal(int64_t T, int32_t H, const int32_t *pos,
+                                      const void *q, const void *k, const void *v,
+                                      int64_t ld_in, void *o, int64_t ld_out, void *stream);
 
 #ifdef __cplusplus
 }

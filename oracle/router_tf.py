@@ -16,7 +16,9 @@ Reading (the paper gives the block's type and sizes, not its wiring):
                                       p = the token's position in its request
   o  = bf16(softmax(q k^T / sqrt(128), causal within the request) v)
   x1 = fp32(x0 + o Wo^T)
-  x2 = fp32(x1 + W2 (silu(W1 m) * W3 m)),  m = bf16(rmsnorm(x1))
+  x2 = fp32(x1 + W2 (silu(W1 m) * W3 m)),  m = bf16(rmsnorm(x1)), the
+                                      hidden product unrounded (as in the
+                                      expert layers' oracle)
   f  = bf16(rmsnorm(x2))
   logits, id = the canonical fp32 gate of ``oracle.route`` on f.
 Sums and products are fp64 here; the roundings to bf16 and fp32 sit where
@@ -130,6 +132,14 @@ def attention_f64(q: np.ndarray, k: np.ndarray, v: np.ndarray,
 def attention(q_bits, k_bits, v_bits, req_offsets) -> np.ndarray:
     """Causal attention on bf16 inputs -> bf16 output."""
     return bf16(attention_f64(_f(q_bits), _f(k_bits), _f(v_bits), req_offsets))
+
+
+def mlp_hidden(m_bits: np.ndarray, w1: np.ndarray, w3: np.ndarray) -> np.ndarray:
+    """The SwiGLU MLP's hidden activations silu(W1 m) * (W3 m), fp64
+    (unrounded), silu(z) = z / (1 + exp(-z)); W2 of this is the MLP's output."""
+    mf = _f(m_bits)
+    g, u = mf @ _f(w1).T, mf @ _f(w3).T
+    return g / (1.0 + np.exp(-g)) * u
 
 
 def router_tf(tokens, req_offsets, emb, wq, wk, wv, wo, w1, w3, w2, w_router, bias,

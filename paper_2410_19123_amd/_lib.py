@@ -82,7 +82,19 @@ SIGNATURES = {
                                     _SZ, _P]),
     "readme_moe_ffn_stack_counts": (_I32, [_I64, _I64, _I32, _I64, _I32, _P, _P, _P, _P, _F,
                                            _P, _SZ, _P]),
+    "readme_router_tf_packed_bytes": (_SZ, [_I64, _I64]),
+    "readme_router_tf_pack": (_I32, [_I64, _I64, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "readme_router_tf_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
+    "readme_router_tf_workspace_offset": (_I64, [_I64, _I64, _I64, _I32]),
+    "readme_router_tf": (_I32, [_I64, _I32, _I64, _I64, _I32, _I64, _P, _P, _P, _P, _P, _P, _F,
+                                _P, _P, _P, _SZ, _P]),
+    "readme_request_positions": (_I32, [_I64, _I32, _P, _P, _P]),
+    "readme_rope": (_I32, [_I64, _I32, _P, _P, _I64, _P]),
+    "readme_attention_causal": (_I32, [_I64, _I32, _P, _P, _P, _P, _I64, _P, _I64, _P]),
 }
+
+# Workspace regions of readme_router_tf (README_RTF_*).
+RTF_REGIONS = ("X", "A", "QKV", "O", "M", "H", "FEAT", "POS", "OFFS")
 
 _lib = None
 
@@ -634,6 +646,115 @@ def readme_moe_ffn_stack(x_resid_grouped, offsets, packed_layers, E, I, rms_eps=
               _p(offsets), pc, _p(x_resid_grouped), float(rms_eps), _p(workspace),
               workspace.numel() * workspace.element_size(), _stream(x_resid_grouped.device))
     return x_resid_grouped
+
+
+def readme_router_tf_packed_bytes(D: int, F: int) -> int:
+    return int(load().readme_router_tf_packed_bytes(D, F))
+
+
+def readme_router_tf_pack(wq, wk, wv, wo, w1, w3, w2, packed=None):
+    """Repack the router block's bf16 weights ([out][in] row-major);
+    returns the packed bytes."""
+    D = wq.shape[0]
+    F = w1.shape[0]
+    for t, shape in ((wq, (D, D)), (wk, (D, D)), (wv, (D, D)), (wo, (D, D)), (w1, (F, D)),
+                     (w3, (F, D)), (w2, (D, F))):
+        if tuple(t.shape) != shape or t.dtype != torch.bfloat16:
+            raise ValueError("router weights must be bf16 [D][D] x4, [F][D] x2, [D][F]")
+    nbytes = readme_router_tf_packed_bytes(D, F)
+    if packed is None:
+        packed = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=wq.device)
+    _dev(wq, wk, wv, wo, w1, w3, w2, packed)
+    _call("readme_router_tf_pack", D, F, _p(wq), _p(wk), _p(wv), _p(wo), _p(w1), _p(w3),
+          _p(w2), _p(packed), packed.numel() * packed.element_size(), _stream(wq.device))
+    return packed
+
+
+def readme_router_tf_workspace_bytes(T: int, D: int, F: int) -> int:
+    return int(load().readme_router_tf_workspace_bytes(T, D, F))
+
+
+def readme_router_tf_workspace_offset(T: int, D: int, F: int, region: str) -> int:
+    return int(load().readme_router_tf_workspace_offset(T, D, F, RTF_REGIONS.index(region)))
+
+
+def readme_router_tf(tokens, req_offsets, emb, packed, F, w_router, bias=None, rms_eps=1e-5,
+                     expert_ids=None, logits=None, workspace=None):
+    """The router G over requests of tokens; returns (expert_ids, logits or
+    None, workspace).  The workspace keeps every intermediate
+    (router_tf_region reads one)."""
+    T = tokens.shape[0]
+    R = req_offsets.shape[0] - 1
+    V, D = emb.shape
+    E = w_router.shape[0]
+    dev = tokens.device
+    if tokens.dtype != torch.int32 or req_offsets.dtype != torch.int32:
+        raise ValueError("tokens and req_offsets must be int32")
+    if emb.dtype != torch.bfloat16 or w_router.dtype != torch.bfloat16 or \
+            w_router.shape[1] != D:
+        raise ValueError("emb [V][D] and w_router [E][D] must be bf16")
+    if bias is not None and (bias.dtype != torch.float32 or bias.numel() != E):
+        raise ValueError("bias must be fp32 [E]")
+    if expert_ids is None:
+        expert_ids = torch.empty(T, dtype=torch.int32, device=dev)
+    ws = readme_router_tf_workspace_bytes(T, D, F)
+    if workspace is None:
+        workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=dev)
+    _dev(tokens, req_offsets, emb, packed, w_router, bias, expert_ids, logits, workspace)
+    _call("readme_router_tf", T, R, D, F, E, V, _p(tokens), _p(req_offsets), _p(emb), _p(packed),
+          _p(w_router), _p(bias), rms_eps, _p(expert_ids), _p(logits), _p(workspace),
+          workspace.numel() * workspace.element_size(), _stream(dev))
+    return expert_ids, logits, workspace
+
+
+def router_tf_region(workspace, T: int, D: int, F: int, region: str):
+    """View of one intermediate in readme_router_tf's workspace."""
+    off = readme_router_tf_workspace_offset(T, D, F, region)
+    Fp = readme_padded_intermediate(F)
+    shape, dt = {"X": ((T, D), torch.float32), "A": ((T, D), torch.bfloat16),
+                 "QKV": ((T, 3 * D), torch.bfloat16), "O": ((T, D), torch.bfloat16),
+                 "M": ((T, D), torch.bfloat16), "H": ((T, Fp), torch.bfloat16),
+                 "FEAT": ((T, D), torch.bfloat16), "POS": ((T,), torch.int32),
+                 "OFFS": ((2,), torch.int32)}[region]
+    n = 1
+    for v in shape:
+        n *= v
+    esz = torch.empty(0, dtype=dt).element_size()
+    return workspace[off:off + n * esz].view(dt).view(shape)
+
+
+def readme_request_positions(req_offsets, T: int, pos=None):
+    """Each token's position in its request; returns pos [T] int32."""
+    R = req_offsets.shape[0] - 1
+    if pos is None:
+        pos = torch.empty(T, dtype=torch.int32, device=req_offsets.device)
+    _dev(req_offsets, pos)
+    _call("readme_request_positions", T, R, _p(req_offsets), _p(pos),
+          _stream(req_offsets.device))
+    return pos
+
+
+def readme_rope(x, pos, H: int):
+    """RoPE in place on H heads of 128 per row of bf16 x [T][ld]; returns x."""
+    T, ld = x.shape
+    if x.dtype != torch.bfloat16:
+        raise ValueError("x must be bf16")
+    _dev(x, pos)
+    _call("readme_rope", T, H, _p(pos), _p(x), ld, _stream(x.device))
+    return x
+
+
+def readme_attention_causal(q, k, v, pos, H: int, o=None):
+    """Causal attention inside each request (bf16 [T][ld], heads of 128)."""
+    T, ld = q.shape
+    if k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("q, k, v shapes disagree")
+    if o is None:
+        o = torch.empty(T, H * 128, dtype=torch.bfloat16, device=q.device)
+    _dev(q, k, v, pos, o)
+    _call("readme_attention_causal", T, H, _p(pos), _p(q), _p(k), _p(v), ld, _p(o), o.shape[1],
+          _stream(q.device))
+    return o
 
 
 def readme_status_string(status: int) -> str:

@@ -69,6 +69,10 @@ hipError_t launch_pack_slots(readme_dtype dt, int64_t E_all, int64_t e0, int64_t
                              int64_t I, const void* wg, const void* wu, const void* wd,
                              int64_t wd_expert_stride, int64_t wd_row_stride, void* packed,
                              hipStream_t s);
+// Rows row0 .. row0+n-1 of a blocked bf16 [N][K] matrix (the packed layout of
+// one expert's down block, N a multiple of 32, K of 64) from row-major src.
+hipError_t launch_pack_rows_bf16(int64_t N, int64_t K, int64_t row0, int64_t n,
+                                 const void* src, int64_t ld, void* packed, hipStream_t s);
 hipError_t launch_grouped_gemm(bool f32, int epi, GemmArgs g, hipStream_t s);
 // Arguments of the two FFN GEMMs over a packed expert buffer (abi.hip).
 GemmArgs gate_up_args(readme_dtype dt, int64_t T, int64_t d, int32_t E, int64_t I,

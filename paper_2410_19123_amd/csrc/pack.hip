@@ -80,6 +80,21 @@ __global__ __launch_bounds__(256) void k_pack_down(int64_t E, int64_t d, int64_t
     }
 }
 
+// Rows row0 .. row0 + n - 1 of a blocked bf16 [N][K] matrix (groups = N / 32
+// row groups) from a row-major source [n][K] with rows ld elements apart.
+__global__ __launch_bounds__(256) void k_pack_rows(int64_t n, int64_t K, int64_t groups,
+                                                   int64_t row0, int64_t ld,
+                                                   const uint16_t* __restrict__ src,
+                                                   char* __restrict__ out) {
+    const int64_t total = n * K;
+    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < total;
+         o += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = o / K, k = o - (o / K) * K;
+        *reinterpret_cast<uint16_t*>(out + blocked_offset(row0 + r, k, groups, 2)) =
+            src[r * ld + k];
+    }
+}
+
 template <typename T>
 static hipError_t pack_t(int64_t E_all, int64_t e0, int64_t n, int64_t d, int64_t I,
                          const void* wg, const void* wu, const void* wd, int64_t es, int64_t rs,
@@ -105,6 +120,16 @@ hipError_t launch_pack_slots(readme_dtype dt, int64_t E_all, int64_t e0, int64_t
                                 packed, s);
     return pack_t<uint16_t>(E_all, e0, n, d, I, wg, wu, wd, wd_expert_stride, wd_row_stride,
                             packed, s);
+}
+
+hipError_t launch_pack_rows_bf16(int64_t N, int64_t K, int64_t row0, int64_t n,
+                                 const void* src, int64_t ld, void* packed, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    const int64_t blocks = ceil_div(n * K, 256);
+    k_pack_rows<<<(unsigned)(blocks < 4096 ? blocks : 4096), 256, 0, s>>>(
+        n, K, N / 32, row0, ld, reinterpret_cast<const uint16_t*>(src),
+        reinterpret_cast<char*>(packed));
+    return hipGetLastError();
 }
 
 hipError_t launch_pack(readme_dtype dt, int64_t E, int64_t d, int64_t I, const void* wg,

@@ -32,6 +32,7 @@ import numpy as np
 
 # Substream tags.
 TAG_X, TAG_ROUTER, TAG_GATE, TAG_UP, TAG_DOWN, TAG_REQ = 1, 2, 3, 4, 5, 6
+TAG_RTF = 7  # the transformer router's weights and tokens (sub-tag in the layer key)
 _CHUNK = 1 << 22
 
 # Logit bias constant for expert 0 of the prefill-scale skewed layer
@@ -308,3 +309,51 @@ __all__ = [
     "router_bias", "make_x", "make_router", "make_request_ids",
     "make_experts", "make_permanent", "make_dense", "make_locality_ids", "make_pool", "flops_per_layer", "describe", "SKEW_BIAS0",
 ]
+
+
+@dataclasses.dataclass(frozen=True)
+class RouterShape:
+    """The pre-gating router G (Table 1): one transformer block of width D
+    (D / 128 heads of 128), SwiGLU MLP width F, vocabulary V, and a gate to
+    E experts."""
+    D: int = 512
+    F: int = 512
+    V: int = 32000
+    E: int = 8
+
+
+# Table 1's router, gating the eight experts of the request batch.
+ROUTER_TABLE1 = RouterShape()
+
+
+def make_router_tf(r: RouterShape, seed: int = 0) -> dict:
+    """Random-init bf16 weights of G ([out][in] row-major bit patterns):
+    emb [V][D] ~ N(0, 1) (rows of the norm's output scale), the projections
+    wq, wk, wv, wo [D][D], w1, w3 [F][D], w2 [D][F] and the gate w_router
+    [E][D] ~ N(0, 0.02).  No gate bias (the block's output sets the load)."""
+    def b(sub, shape, std):
+        return to_bf16_bits(normal(shape, std, [seed, TAG_RTF, sub]))
+    D, F = r.D, r.F
+    return dict(emb=b(1, (r.V, D), 1.0), wq=b(2, (D, D), 0.02), wk=b(3, (D, D), 0.02),
+                wv=b(4, (D, D), 0.02), wo=b(5, (D, D), 0.02), w1=b(6, (F, D), 0.02),
+                w3=b(7, (F, D), 0.02), w2=b(8, (D, F), 0.02), w_router=b(9, (r.E, D), 0.02),
+                bias=None)
+
+
+def make_router_requests(lengths, V: int, seed: int = 0):
+    """Token ids uniform over [0, V) for requests of the given lengths
+    (zero allowed); returns (tokens [T] int32, req_offsets [R+1] int32)."""
+    lengths = np.asarray(lengths, dtype=np.int64)
+    offs = np.zeros(len(lengths) + 1, np.int64)
+    np.cumsum(lengths, out=offs[1:])
+    rng = np.random.default_rng([seed, TAG_RTF, 100, 0])
+    tokens = rng.integers(0, V, size=int(offs[-1])).astype(np.int32)
+    return tokens, offs.astype(np.int32)
+
+
+def ragged_lengths(T: int, R: int, seed: int = 0):
+    """R request lengths summing to T, cut at R - 1 uniform points (so some
+    may be zero and a few long)."""
+    rng = np.random.default_rng([seed, TAG_RTF, 101, 0])
+    cuts = np.sort(rng.integers(0, T + 1, size=R - 1))
+    return np.diff(np.concatenate([[0], cuts, [T]])).astype(np.int64)

@@ -183,6 +183,57 @@ def test_streamed_buffers_checked_before_any_launch(lib):
     assert t(1, 16, 4096, 8, 1376, 2, odd, FAKE, FAKE, FAKE, FAKE, FAKE, big, None) == 1
 
 
+def test_router_tf_sizes_and_errors(lib):
+    D, F = 512, 512
+    assert lib.readme_router_tf_packed_bytes(D, F) == 4 * D * D * 2 + 3 * F * D * 2
+    assert lib.readme_router_tf_packed_bytes(500, F) == 0          # heads of 128
+    assert lib.readme_router_tf_packed_bytes(D, 0) == 0
+    T = 100
+    sizes = [T * D * 4, T * D * 2, T * 3 * D * 2, T * D * 2, T * D * 2, T * F * 2, T * D * 2,
+             T * 4, 8]
+    off = 0
+    for region, n in enumerate(sizes):
+        assert lib.readme_router_tf_workspace_offset(T, D, F, region) == off
+        off += (n + 255) // 256 * 256
+    assert lib.readme_router_tf_workspace_offset(T, D, F, len(sizes)) == off
+    assert lib.readme_router_tf_workspace_bytes(T, D, F) == off
+    assert lib.readme_router_tf_workspace_offset(T, D, F, len(sizes) + 1) == -1
+    assert lib.readme_router_tf_workspace_offset(-1, D, F, 0) == -1
+    assert lib.readme_router_tf_workspace_bytes(T, 384, 100) > 0   # F padded to 128
+    r = lib.readme_router_tf
+    eps = ctypes.c_float(1e-5)
+    ws = 1 << 40
+    args = lambda **k: [k.get("T", 64), k.get("R", 2), k.get("D", 512), k.get("F", 512),
+                        k.get("E", 8), k.get("V", 32000), FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                        k.get("eps", eps), FAKE, None, k.get("ws", FAKE),
+                        k.get("wsb", ws), None]
+    assert r(*args(D=500)) == 2
+    assert r(*args(D=16384 + 128)) == 2
+    assert r(*args(E=0)) == 2
+    assert r(*args(E=257)) == 2
+    assert r(*args(R=0)) == 1
+    assert r(*args(V=0)) == 1
+    assert r(*args(eps=ctypes.c_float(-1.0))) == 1
+    assert r(*args(wsb=10)) == 3
+    assert r(*args(ws=ctypes.c_void_p(4100))) == 1
+    assert r(*args(T=0, R=0)) == 0
+    pk = lib.readme_router_tf_pack
+    assert pk(512, 512, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 10, None) == 3
+    assert pk(512, 512, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == 1
+    assert pk(640, 0, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == 1
+    at = lib.readme_attention_causal
+    assert at(10, 2, FAKE, FAKE, FAKE, FAKE, 200, FAKE, 256, None) == 1      # ld_in < 256
+    assert at(10, 2, FAKE, FAKE, FAKE, FAKE, 260, FAKE, 256, None) == 1      # ld_in % 8
+    assert at(10, 2, FAKE, ctypes.c_void_p(4104), FAKE, FAKE, 256, FAKE, 256, None) == 1
+    assert at(0, 2, None, None, None, None, 256, None, 256, None) == 0
+    ro = lib.readme_rope
+    assert ro(10, 2, FAKE, FAKE, 255, None) == 1
+    assert ro(0, 2, None, None, 256, None) == 0
+    rp = lib.readme_request_positions
+    assert rp(10, 0, FAKE, FAKE, None) == 1
+    assert rp(0, 0, None, None, None) == 0
+
+
 def test_tile_override_is_per_thread(lib):
     import threading
     assert lib.readme_set_gemm_tile(32) == 1

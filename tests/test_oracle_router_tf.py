@@ -136,3 +136,19 @@ def test_embedding_of_out_of_range_ids_is_zero():
     x = R.embed(np.array([0, -1, 10, 9]), emb)
     assert np.all(x[1] == 0) and np.all(x[2] == 0)
     assert np.array_equal(x[3], R._f(emb[9]).astype(np.float32))
+
+
+def test_mlp_hidden_agrees_with_the_layer_oracle(oracle_mod):
+    """W2 mlp_hidden(m) is the C oracle's FFN layer output on the same
+    residual rows (one expert covering every row)."""
+    rng = np.random.default_rng(7)
+    D, F, T = 128, 96, 5
+    x = rng.standard_normal((T, D)).astype(np.float32)
+    w1, w3 = (R.bf16(rng.standard_normal((F, D)) * 0.05) for _ in range(2))
+    w2 = R.bf16(rng.standard_normal((D, F)) * 0.05)
+    m = R.rmsnorm_bf16(x)
+    ours = R.mlp_hidden(m, w1, w3) @ R._f(w2).T
+    ref, xn = oracle_mod.layer(x, np.array([0, T], np.int32), w1[None], w3[None], w2[None],
+                               want_xn=True)
+    assert np.array_equal(xn, m)
+    assert np.allclose(ours, ref, rtol=1e-12, atol=1e-12)
