@@ -68,6 +68,9 @@ def parse():
     ap.add_argument("--library-gemm", action="store_true",
                     help="also time the same per-expert GEMMs with torch's library GEMM "
                          "(context for the grouped kernels; not part of the path)")
+    ap.add_argument("--router-only", action="store_true",
+                    help="time only the pre-gating router G (Table 1) on the request "
+                         "batch's tokens and print its line")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
@@ -652,6 +655,66 @@ def side_line(name: str, K: int, W: int) -> dict:
     return out
 
 
+def router_flops(shape: wl.RouterShape, lengths) -> float:
+    """Algorithmic FLOP of one router call: the projections (q, k, v, o:
+    8 D^2 per token), the SwiGLU MLP (6 D F), the gate (2 D E) and causal
+    attention (4 * 128 * prefix length per token and head, D / 128 heads)."""
+    D, F, E = shape.D, shape.F, shape.E
+    T = int(np.sum(lengths))
+    prefix = sum(n * (n + 1) // 2 for n in lengths)
+    return T * (8.0 * D * D + 6.0 * D * F + 2.0 * D * E) + 4.0 * 128 * prefix * (D // 128)
+
+
+def router_line(K: int, W: int) -> dict:
+    """The pre-gating router G (Sec. 2.3, Table 1: one causal transformer
+    block of width 512, four heads, SwiGLU MLP 512, vocabulary 32000, then
+    the gate to 8 experts) over the request batch's tokens, 256 requests x
+    32 tokens, random-init weights.  One call = embedding, block, gate, all
+    on the GPU; HIP events on the launch stream around K calls."""
+    import torch
+    from paper_2410_19123_amd import _lib as L
+    shape = wl.ROUTER_TABLE1
+    lengths = [32] * 256
+    wts = wl.make_router_tf(shape, 0)
+    tokens, ro = wl.make_router_requests(lengths, shape.V, 0)
+    dev = torch.device("cuda:0")
+    dw = {n: L.to_device(wts[n], dev) for n in ("emb", "wq", "wk", "wv", "wo", "w1", "w3", "w2",
+                                                "w_router")}
+    packed = L.readme_router_tf_pack(dw["wq"], dw["wk"], dw["wv"], dw["wo"], dw["w1"],
+                                     dw["w3"], dw["w2"])
+    tk, rof = L.to_device(tokens, dev), L.to_device(ro, dev)
+    T = len(tokens)
+    ids = torch.empty(T, dtype=torch.int32, device=dev)
+    logits = torch.empty(T, shape.E, dtype=torch.float32, device=dev)
+    ws = torch.empty(L.readme_router_tf_workspace_bytes(T, shape.D, shape.F), dtype=torch.uint8,
+                     device=dev)
+
+    def call():
+        L.readme_router_tf(tk, rof, dw["emb"], packed, shape.F, dw["w_router"], None, 1e-5,
+                           expert_ids=ids, logits=logits, workspace=ws)
+
+    for _ in range(W):
+        call()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(K):
+        call()
+    t1.record()
+    torch.cuda.synchronize()
+    us = t0.elapsed_time(t1) * 1e3 / K
+    fl = router_flops(shape, lengths)
+    counts = np.bincount(L.from_device(ids), minlength=shape.E)
+    out = {"workload": "router_tf_table1_requests_256x32", "T": T, "D": shape.D, "F": shape.F,
+           "V": shape.V, "E": shape.E, "heads": shape.D // 128, "requests": len(lengths),
+           "steps": K, "us_per_call": round(us, 2), "tokens_per_s": round(T / (us * 1e-6), 1),
+           "gflop_per_call": round(fl / 1e9, 3), "tflops": round(fl / (us * 1e-6) / 1e12, 2),
+           "tokens_per_expert": counts.tolist()}
+    del dw, packed, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -663,6 +726,10 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
+
+    if args.router_only:
+        print(json.dumps({"router": router_line(args.steps, args.warmup)}), flush=True)
+        return
 
     w = wl.WORKLOADS[args.workload]
     if (w.P or w.K > 1) and args.unfused:
@@ -747,6 +814,7 @@ def main():
     if not args.no_side and args.workload not in ("llama7b_decode32", "prefill_skew16"):
         out["decode"] = side_line("llama7b_decode32", args.side_steps, 3)
         out["prefill"] = side_line("prefill_skew16", args.side_steps, 3)
+        out["router"] = router_line(args.side_steps, 3)
     if args.library_gemm and w.dtype == "bf16" and w.layers == 1 and w.K == 1 and not w.P:
         out["library_gemm"] = library_gemm(w, counts)
     if not args.no_cpu_baseline:

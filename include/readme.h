@@ -732,7 +732,8 @@ readme_status readme_request_positions(int64_t T, int32_t R, const int32_t *req_
  *   x_{i+64} <- x_{i+64} cos + x_i sin
  * (the rotate-half form), angle, sine, cosine and products in fp64 without
  * fused multiply-adds, each result rounded to fp32 and then to bf16 (nearest
- * even).  pos [T] int32 (readme_request_positions).  Requires ld >= 128 H.
+ * even).  pos [T] int32 (readme_request_positions).  Requires ld >= 128 H,
+ * ld a multiple of 8 and x 16-byte aligned.
  */
 readme_status readme_rope(int64_t T, int32_t H, const int32_t *pos, void *x, int64_t ld,
                           void *stream);

@@ -32,6 +32,7 @@ int get_gemm_tile() { return t_forced_tile; }
 static int tile_by_shape(bool f32, bool gate_up, const GemmArgs& g) {
     const int f = forced_tile();
     if (f > 0) return f;
+    if (g.tile > TILE_AUTO && g.tile <= TILE_LAST) return g.tile;
     const int64_t per_expert = g.T / (g.E > 0 ? g.E : 1);
     if (f32) {  // both operands through LDS (the register-streamed kernels are bf16 only)
         if (per_expert >= (gate_up ? 768 : 192)) return TILE_256x256;

@@ -47,6 +47,9 @@ struct GemmArgs {
     // m_tiles32 > 0: sum over experts of ceil(rows_e / 32), from token counts
     // the caller knows on the host (the tile choice then sees the split).
     int m_tiles32;
+    // tile > 0: this launch's tile configuration (a caller that measured its
+    // own shapes); the calling thread's override still takes precedence.
+    int tile;
     int n_tiles, m_tiles_max; // filled by the launcher
     // Tiles of several heights in one launch: the block range of class c is
     // [mix_start[c], mix_start[c+1]) (filled by the launcher).

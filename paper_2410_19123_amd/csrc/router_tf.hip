@@ -14,8 +14,9 @@
 //   x += W2 (silu(W1 m) * W3 m),  m = bf16(rmsnorm(x))
 //   f  = bf16(rmsnorm(x));  ids, logits = gate(f)
 // The projections and the MLP run on the grouped-GEMM kernels with one
-// "expert" (offsets {0, T}); the norms and the gate reuse the FFN stack's
-// kernels.  New here: the embedding gather, RoPE and causal attention.
+// "expert" (offsets {0, T}).  Here: the embedding gather fused with the
+// first norm, the MLP's norm, RoPE, causal attention, and the final norm
+// fused with the gate (readme_route's canonical fp32 order).  Seven launches.
 #include <limits.h>
 #include <math.h>
 
@@ -29,6 +30,11 @@ namespace {
 constexpr int kHeadDim = 128;
 // log2(e) / sqrt(128): scores go to exp2 in one multiply.
 constexpr float kScoreScale = 0.12751743082459868f;
+// Waves (of 32 queries each) per attention workgroup: one, so that a wave
+// loops only over its own queries' key blocks (a request batch of short
+// requests then needs one key block per wave) and no wave waits at another's
+// barrier.
+constexpr int kAttnWaves = 1;
 
 // First token of t's request, from the in-request position (clamped, so a
 // malformed position never leads outside [0, t]).
@@ -55,31 +61,202 @@ __device__ __forceinline__ int32_t position_of(int64_t t, int32_t R,
     return (int32_t)(t - start);
 }
 
-// x[t] = fp32(emb[tokens[t]]) (zeros outside [0, V)), 8 elements per thread;
-// the first chunk's thread also writes pos[t], thread 0 the offsets {0, T}
-// of the one-group GEMM launches.
-__global__ __launch_bounds__(256) void k_embed(int64_t T, int64_t D, int32_t R, int64_t V,
-                                               const int32_t* __restrict__ tokens,
-                                               const int32_t* __restrict__ ro,
-                                               const uint16_t* __restrict__ emb,
-                                               float* __restrict__ x, int32_t* __restrict__ pos,
-                                               int32_t* __restrict__ offs) {
-    const int64_t n8 = D / 8, total = T * n8;
-    const int64_t first = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (first == 0) {
+// Request offsets staged in LDS for the position search when they fit.
+constexpr int kRoLds = 4096;
+
+// Sum over the wave to lane 0 in a fixed order, then broadcast, so that every
+// lane holds the same fp32 total.
+__device__ __forceinline__ float wave_sum_bcast(float v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_down(v, off, 64);
+    return __shfl(v, 0, 64);
+}
+
+// Embedding and the pre-attention norm, one wave per token (four per
+// workgroup): x[t] = fp32(emb[tokens[t]]) (zeros for an id outside [0, V)),
+// a[t] = bf16(x[t] * r), r = 1 / sqrt(mean x^2 + eps) in fp32 (each lane sums
+// its elements in ascending order, then the wave folds).  Lane l owns the
+// 8-element chunks l, l + 64, ...; the row is read once more from the
+// (cached) table for the second pass.  Lane 0 writes pos[t], found by binary
+// search over the request offsets (staged in LDS when R + 1 <= 4096);
+// thread 0 of block 0 writes the offsets {0, T} of the one-group GEMMs.
+__global__ __launch_bounds__(256) void k_embed_norm(int64_t T, int64_t D, int32_t R, int64_t V,
+                                                    float eps,
+                                                    const int32_t* __restrict__ tokens,
+                                                    const int32_t* __restrict__ ro,
+                                                    const uint16_t* __restrict__ emb,
+                                                    float* __restrict__ x,
+                                                    uint16_t* __restrict__ a,
+                                                    int32_t* __restrict__ pos,
+                                                    int32_t* __restrict__ offs) {
+    __shared__ int32_t ro_lds[kRoLds];
+    const bool staged = R + 1 <= kRoLds;
+    if (staged)
+        for (int i = threadIdx.x; i <= R; i += blockDim.x) ro_lds[i] = ro[i];
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
         offs[0] = 0;
         offs[1] = (int32_t)T;
     }
-    for (int64_t i = first; i < total; i += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t t = i / n8, c = i - t * n8;
-        const int64_t tok = tokens[t];
+    __syncthreads();
+    const int lane = threadIdx.x & 63;
+    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (t >= T) return;
+    if (lane == 0) pos[t] = position_of(t, R, staged ? ro_lds : ro);
+    const int64_t tok = tokens[t];
+    const bool ok = tok >= 0 && tok < V;
+    const uint16_t* er = emb + (ok ? tok : 0) * D;
+    const int64_t nch = D / 8;
+    float ss = 0.0f;
+    for (int64_t c = lane; c < nch; c += 64) {
         uint4 w = make_uint4(0u, 0u, 0u, 0u);
-        if (tok >= 0 && tok < V) w = *reinterpret_cast<const uint4*>(emb + tok * D + c * 8);
+        if (ok) w = *reinterpret_cast<const uint4*>(er + c * 8);
+        const float v[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
+                            bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
         float4* dst = reinterpret_cast<float4*>(x + t * D + c * 8);
-        dst[0] = make_float4(bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y));
-        dst[1] = make_float4(bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w));
-        if (c == 0) pos[t] = position_of(t, R, ro);
+        dst[0] = make_float4(v[0], v[1], v[2], v[3]);
+        dst[1] = make_float4(v[4], v[5], v[6], v[7]);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) ss += v[k] * v[k];
     }
+    const float r = 1.0f / sqrtf(wave_sum_bcast(ss) / (float)D + eps);
+    for (int64_t c = lane; c < nch; c += 64) {
+        uint4 w = make_uint4(0u, 0u, 0u, 0u);
+        if (ok) w = *reinterpret_cast<const uint4*>(er + c * 8);
+        uint4 o;
+        o.x = (uint32_t)f32_to_bf16(bf16_lo(w.x) * r) | ((uint32_t)f32_to_bf16(bf16_hi(w.x) * r) << 16);
+        o.y = (uint32_t)f32_to_bf16(bf16_lo(w.y) * r) | ((uint32_t)f32_to_bf16(bf16_hi(w.y) * r) << 16);
+        o.z = (uint32_t)f32_to_bf16(bf16_lo(w.z) * r) | ((uint32_t)f32_to_bf16(bf16_hi(w.z) * r) << 16);
+        o.w = (uint32_t)f32_to_bf16(bf16_lo(w.w) * r) | ((uint32_t)f32_to_bf16(bf16_hi(w.w) * r) << 16);
+        *reinterpret_cast<uint4*>(a + t * D + c * 8) = o;
+    }
+}
+
+// m[t] = bf16(x[t] * r), r as above; one wave per row, lane l owning the
+// 4-element chunks l, l + 64, ... (the row read twice, the second time from
+// cache).
+__global__ __launch_bounds__(256) void k_rms_rows(int64_t T, int64_t D, float eps,
+                                                  const float* __restrict__ x,
+                                                  uint16_t* __restrict__ m) {
+    const int lane = threadIdx.x & 63;
+    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (t >= T) return;
+    const float4* row = reinterpret_cast<const float4*>(x + t * D);
+    const int64_t n4 = D / 4;
+    float ss = 0.0f;
+    for (int64_t c = lane; c < n4; c += 64) {
+        const float4 v = row[c];
+        ss += v.x * v.x;
+        ss += v.y * v.y;
+        ss += v.z * v.z;
+        ss += v.w * v.w;
+    }
+    const float r = 1.0f / sqrtf(wave_sum_bcast(ss) / (float)D + eps);
+    uint2* out = reinterpret_cast<uint2*>(m + t * D);
+    for (int64_t c = lane; c < n4; c += 64) {
+        const float4 v = row[c];
+        uint2 o;
+        o.x = (uint32_t)f32_to_bf16(v.x * r) | ((uint32_t)f32_to_bf16(v.y * r) << 16);
+        o.y = (uint32_t)f32_to_bf16(v.z * r) | ((uint32_t)f32_to_bf16(v.w * r) << 16);
+        out[c] = o;
+    }
+}
+
+// The final norm and the gate in one pass, one wave per token, for D <= 2048
+// (at most NC = 4 chunks of 8 per lane, held in registers):
+//   f[t] = bf16(x[t] * r)                         (written out)
+//   logit[t][e] = canonical fp32 sum of f[t][k] * w_router[e][k] + bias[e]
+// The canonical order (the one readme_route follows): 16-byte chunks of f and
+// w_router (8 bf16 values), chunk c to partial c mod 64 -- here lane c mod
+// 64 -- each partial fusing multiply-adds in ascending k from +0, the 64
+// partials folded pairwise (p[l] += p[l + off], off = 32 .. 1), then the
+// bias added.  id = first e of largest logit (strict '>' from e = 0).
+template <int NC>
+__global__ __launch_bounds__(256) void k_norm_gate(int64_t T, int64_t D, int E, float eps,
+                                                   const float* __restrict__ x,
+                                                   const uint16_t* __restrict__ w,
+                                                   const float* __restrict__ bias,
+                                                   uint16_t* __restrict__ f,
+                                                   int32_t* __restrict__ ids,
+                                                   float* __restrict__ logits) {
+    const int lane = threadIdx.x & 63;
+    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (t >= T) return;
+    const int nch = (int)(D / 8);
+    float v[NC][8];
+    float ss = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+        const int c = lane + 64 * j;
+        if (c < nch) {
+            const float4* src = reinterpret_cast<const float4*>(x + t * D + (int64_t)c * 8);
+            const float4 p0 = src[0], p1 = src[1];
+            v[j][0] = p0.x; v[j][1] = p0.y; v[j][2] = p0.z; v[j][3] = p0.w;
+            v[j][4] = p1.x; v[j][5] = p1.y; v[j][6] = p1.z; v[j][7] = p1.w;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) ss += v[j][k] * v[j][k];
+        }
+    }
+    const float r = 1.0f / sqrtf(wave_sum_bcast(ss) / (float)D + eps);
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+        const int c = lane + 64 * j;
+        if (c < nch) {
+            uint16_t b[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                b[k] = f32_to_bf16(v[j][k] * r);
+                v[j][k] = bf16_lo(b[k]);
+            }
+            uint4 o;
+            o.x = (uint32_t)b[0] | ((uint32_t)b[1] << 16);
+            o.y = (uint32_t)b[2] | ((uint32_t)b[3] << 16);
+            o.z = (uint32_t)b[4] | ((uint32_t)b[5] << 16);
+            o.w = (uint32_t)b[6] | ((uint32_t)b[7] << 16);
+            *reinterpret_cast<uint4*>(f + t * D + (int64_t)c * 8) = o;
+        }
+    }
+    // Eight experts at a time, so that their partial sums and pairwise folds
+    // proceed side by side.
+    int best_e = 0;
+    float best = 0.0f;
+    for (int e0 = 0; e0 < E; e0 += 8) {
+        float p[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) p[i] = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int e = e0 + i < E ? e0 + i : E - 1;   // clamped rows are not used
+#pragma unroll
+            for (int j = 0; j < NC; ++j) {
+                const int c = lane + 64 * j;
+                if (c < nch) {
+                    const uint4 wv =
+                        *reinterpret_cast<const uint4*>(w + (int64_t)e * D + (int64_t)c * 8);
+                    const float wf[8] = {bf16_lo(wv.x), bf16_hi(wv.x), bf16_lo(wv.y),
+                                         bf16_hi(wv.y), bf16_lo(wv.z), bf16_hi(wv.z),
+                                         bf16_lo(wv.w), bf16_hi(wv.w)};
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) p[i] = fmaf(v[j][k], wf[k], p[i]);
+                }
+            }
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) p[i] = p[i] + __shfl_down(p[i], off, 64);
+        if (lane == 0) {
+            for (int i = 0; i < 8 && e0 + i < E; ++i) {
+                const int e = e0 + i;
+                const float lg = bias ? p[i] + bias[e] : p[i];
+                if (logits) logits[t * E + e] = lg;
+                if (e == 0 || lg > best) {
+                    best = lg;
+                    best_e = e;
+                }
+            }
+        }
+    }
+    if (lane == 0) ids[t] = best_e;
 }
 
 __global__ __launch_bounds__(256) void k_positions(int64_t T, int32_t R,
@@ -91,30 +268,61 @@ __global__ __launch_bounds__(256) void k_positions(int64_t T, int32_t R,
 }
 
 // RoPE in place on NH heads of 128 bf16 values per row (row t at x + t*ld).
-// One thread per (token, pair index i): the angle and its cosine and sine
-// in fp64, the rotation of each head's pair (i, i + 64) in fp64 without
-// fused multiply-adds, then the round to fp32 and to bf16 (nearest even).
+// One thread per (token, pair indices i0 and i0 + 1): per i the angle
+// pos[t] * 10000^(-2i/128) and its cosine and sine in fp64 (the 64 inverse
+// frequencies computed once per workgroup), then for each head the 4-byte
+// runs (x_i0, x_i0+1) and (x_i0+64, x_i0+65), each pair rotated in fp64
+// without fused multiply-adds and rounded to fp32 and then to bf16 (nearest
+// even).  Two pairs per thread keep four waves per SIMD for the fp64 sine
+// and cosine.
 __global__ __launch_bounds__(256) void k_rope(int64_t T, int NH,
                                               const int32_t* __restrict__ pos,
                                               uint16_t* __restrict__ x, int64_t ld) {
 #pragma clang fp contract(off)
+    __shared__ double inv_lds[64];
+    if (threadIdx.x < 64)
+        inv_lds[threadIdx.x] = pow(10000.0, -2.0 * (double)threadIdx.x / (double)kHeadDim);
+    __syncthreads();
     const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (g >= T * 64) return;
-    const int64_t t = g >> 6;
-    const int i = (int)(g & 63);
-    const double inv = pow(10000.0, -2.0 * (double)i / (double)kHeadDim);
-    const double ang = (double)pos[t] * inv;
-    double sn, cs;
-    sincos(ang, &sn, &cs);
-    uint16_t* row = x + t * ld;
-    for (int hh = 0; hh < NH; ++hh) {
-        uint16_t* p = row + (int64_t)hh * kHeadDim;
-        const double a = (double)bf16_lo(p[i]);
-        const double b = (double)bf16_lo(p[i + 64]);
-        const double ra = a * cs - b * sn;
-        const double rb = b * cs + a * sn;
-        p[i] = f32_to_bf16((float)ra);
-        p[i + 64] = f32_to_bf16((float)rb);
+    if (g >= T * 32) return;
+    const int64_t t = g >> 5;
+    const int i0 = (int)(g & 31) * 2;
+    const double p = (double)pos[t];
+    double cs[2], sn[2];
+    sincos(p * inv_lds[i0], &sn[0], &cs[0]);
+    sincos(p * inv_lds[i0 + 1], &sn[1], &cs[1]);
+    uint16_t* row = x + t * ld + i0;
+    // Heads in batches of 8: every load of a batch is issued before its
+    // first store (a store could alias a later head's load otherwise, which
+    // would serialise the loads).
+    for (int h0 = 0; h0 < NH; h0 += 8) {
+        const int nb = NH - h0 < 8 ? NH - h0 : 8;
+        uint32_t wa[8], wb[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (j < nb) {
+                const uint16_t* lo = row + (int64_t)(h0 + j) * kHeadDim;
+                wa[j] = *reinterpret_cast<const uint32_t*>(lo);
+                wb[j] = *reinterpret_cast<const uint32_t*>(lo + 64);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (j >= nb) continue;
+            uint32_t oa = 0, ob = 0;
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                const double av = (double)(k ? bf16_hi(wa[j]) : bf16_lo(wa[j]));
+                const double bv = (double)(k ? bf16_hi(wb[j]) : bf16_lo(wb[j]));
+                const double xa = av * cs[k] - bv * sn[k];
+                const double xb = bv * cs[k] + av * sn[k];
+                oa |= (uint32_t)f32_to_bf16((float)xa) << (16 * k);
+                ob |= (uint32_t)f32_to_bf16((float)xb) << (16 * k);
+            }
+            uint16_t* lo = row + (int64_t)(h0 + j) * kHeadDim;
+            *reinterpret_cast<uint32_t*>(lo) = oa;
+            *reinterpret_cast<uint32_t*>(lo + 64) = ob;
+        }
     }
 }
 
@@ -137,10 +345,12 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 //   o = O / l, rounded to bf16.  Key blocks run from the first query's
 //   request start to the last query; a wave skips the blocks outside its own
 //   queries' range (the workgroup still passes every barrier).
-__global__ __launch_bounds__(256) void k_attention_causal(
-    int64_t T, const int32_t* __restrict__ pos, const uint16_t* __restrict__ q,
-    const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, int64_t ldi,
-    uint16_t* __restrict__ o, int64_t ldo) {
+template <int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void k_attention_causal(int64_t T, const int32_t* __restrict__ pos,
+                        const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+                        const uint16_t* __restrict__ v, int64_t ldi, uint16_t* __restrict__ o,
+                        int64_t ldo) {
     constexpr int KP = kHeadDim + 8;  // K rows in LDS, 272 bytes apart
     constexpr int VP = 32 + 8;        // V^T rows (one per dim), 80 bytes apart
     __shared__ __attribute__((aligned(16))) uint16_t k_lds[32 * KP];
@@ -149,7 +359,7 @@ __global__ __launch_bounds__(256) void k_attention_causal(
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int hf = lane >> 5, col = lane & 31;
     const int64_t hoff = (int64_t)blockIdx.y * kHeadDim;
-    const int64_t q0 = (int64_t)blockIdx.x * 128;
+    const int64_t q0 = (int64_t)blockIdx.x * (32 * NW);
     const int64_t t = q0 + 32 * wv + col;
     const bool tv = t < T;
     const int64_t tq = tv ? t : T - 1;
@@ -159,7 +369,7 @@ __global__ __launch_bounds__(256) void k_attention_causal(
     const int64_t wlo = request_start(wact ? wfirst : T - 1, pos);
     const int64_t whi = wfirst + 31 < T - 1 ? wfirst + 31 : T - 1;
     const int64_t lo = request_start(q0, pos);
-    const int64_t hi = q0 + 127 < T - 1 ? q0 + 127 : T - 1;
+    const int64_t hi = q0 + 32 * NW - 1 < T - 1 ? q0 + 32 * NW - 1 : T - 1;
 
     bf16x8 qf[8];
     {
@@ -176,7 +386,7 @@ __global__ __launch_bounds__(256) void k_attention_causal(
 
     for (int64_t kb = lo >> 5; kb <= (hi >> 5); ++kb) {
         const int64_t k0 = kb * 32;
-        for (int c = tid; c < 32 * (kHeadDim / 8); c += 256) {
+        for (int c = tid; c < 32 * (kHeadDim / 8); c += 64 * NW) {
             const int r = c >> 4, ch = c & 15;
             const int64_t key = k0 + r;
             uint4 kv = make_uint4(0u, 0u, 0u, 0u), vv = kv;
@@ -281,11 +491,39 @@ unsigned grid_of(int64_t n, int64_t cap) {
     return (unsigned)(b < 1 ? 1 : (b > cap ? cap : b));
 }
 
-hipError_t launch_embed(int64_t T, int64_t D, int32_t R, int64_t V, const int32_t* tokens,
-                        const int32_t* ro, const void* emb, float* x, int32_t* pos,
-                        int32_t* offs, hipStream_t s) {
-    k_embed<<<grid_of(T * (D / 8), 1 << 16), 256, 0, s>>>(
-        T, D, R, V, tokens, ro, reinterpret_cast<const uint16_t*>(emb), x, pos, offs);
+hipError_t launch_embed_norm(int64_t T, int64_t D, int32_t R, int64_t V, float eps,
+                             const int32_t* tokens, const int32_t* ro, const void* emb,
+                             float* x, uint16_t* a, int32_t* pos, int32_t* offs,
+                             hipStream_t s) {
+    k_embed_norm<<<(unsigned)ceil_div(T, 4), 256, 0, s>>>(
+        T, D, R, V, eps, tokens, ro, reinterpret_cast<const uint16_t*>(emb), x, a, pos, offs);
+    return hipGetLastError();
+}
+
+hipError_t launch_rms_rows(int64_t T, int64_t D, float eps, const float* x, uint16_t* m,
+                           hipStream_t s) {
+    k_rms_rows<<<(unsigned)ceil_div(T, 4), 256, 0, s>>>(T, D, eps, x, m);
+    return hipGetLastError();
+}
+
+// Final norm + gate: fused for D <= 2048, else the norm then readme_route's
+// kernel (the same canonical gate).
+hipError_t launch_norm_gate(int64_t T, int64_t D, int E, float eps, const float* x,
+                            const void* w, const float* bias, uint16_t* f, int32_t* ids,
+                            float* logits, hipStream_t s) {
+    const unsigned grid = (unsigned)ceil_div(T, 4);
+    const uint16_t* wb = reinterpret_cast<const uint16_t*>(w);
+    if (D <= 512)
+        k_norm_gate<1><<<grid, 256, 0, s>>>(T, D, E, eps, x, wb, bias, f, ids, logits);
+    else if (D <= 1024)
+        k_norm_gate<2><<<grid, 256, 0, s>>>(T, D, E, eps, x, wb, bias, f, ids, logits);
+    else if (D <= 2048)
+        k_norm_gate<4><<<grid, 256, 0, s>>>(T, D, E, eps, x, wb, bias, f, ids, logits);
+    else {
+        hipError_t e = launch_rms_rows(T, D, eps, x, f, s);
+        if (e != hipSuccess) return e;
+        return launch_route(README_BF16, T, D, E, f, w, bias, ids, logits, s);
+    }
     return hipGetLastError();
 }
 
@@ -297,19 +535,28 @@ hipError_t launch_positions(int64_t T, int32_t R, const int32_t* ro, int32_t* po
 
 hipError_t launch_rope(int64_t T, int NH, const int32_t* pos, void* x, int64_t ld,
                        hipStream_t s) {
-    k_rope<<<(unsigned)ceil_div(T * 64, 256), 256, 0, s>>>(T, NH, pos,
+    k_rope<<<(unsigned)ceil_div(T * 32, 256), 256, 0, s>>>(T, NH, pos,
                                                           reinterpret_cast<uint16_t*>(x), ld);
     return hipGetLastError();
 }
 
 hipError_t launch_attention(int64_t T, int H, const int32_t* pos, const void* q, const void* k,
                             const void* v, int64_t ldi, void* o, int64_t ldo, hipStream_t s) {
-    const dim3 grid((unsigned)ceil_div(T, 128), (unsigned)H);
-    k_attention_causal<<<grid, 256, 0, s>>>(
+    const dim3 grid((unsigned)ceil_div(T, 32 * kAttnWaves), (unsigned)H);
+    k_attention_causal<kAttnWaves><<<grid, 64 * kAttnWaves, 0, s>>>(
         T, pos, reinterpret_cast<const uint16_t*>(q), reinterpret_cast<const uint16_t*>(k),
         reinterpret_cast<const uint16_t*>(v), ldi, reinterpret_cast<uint16_t*>(o), ldo);
     return hipGetLastError();
 }
+
+// Tile configurations (TILE_* of the grouped GEMM) of the block's GEMMs
+// from a sweep of all tiles at 8192 tokens, D = F = 512: q|k|v (N = 3D)
+// 27.4 us with the eight-wave 256-row tiles, o and down (N = D) 15.6 -
+// 16.3 us with 64 x 256 four-wave tiles against 28 us automatic, gate/up
+// (N = 2F) 18.2 us with 128 x 256 LDS tiles against 28.6.
+constexpr int kTileQkv = 30;     // TILE_MIX8_256
+constexpr int kTileNarrow = 13;  // TILE_BD_64x256
+constexpr int kTileGateUp = 4;   // TILE_128x256
 
 // C[T][ldc] (+)= A[T][K] W^T over one group of all T rows, W a blocked bf16
 // [N][K] matrix.
@@ -421,7 +668,7 @@ readme_status readme_rope(int64_t T, int32_t H, const int32_t* pos, void* x, int
     if (T < 0 || H < 0 || ld < (int64_t)H * kHeadDim) return README_ERR_ARG;
     if (T > INT32_MAX) return README_ERR_UNSUPPORTED;
     if (T == 0 || H == 0) return README_OK;
-    if (!pos || !x) return README_ERR_ARG;
+    if (!pos || !x || !al16(x) || ld % 8) return README_ERR_ARG;
     return st_of(launch_rope(T, H, pos, x, ld, as_stream(stream)));
 }
 
@@ -470,32 +717,41 @@ readme_status readme_router_tf(int64_t T, int32_t R, int64_t D, int64_t F, int32
     const char* pk = reinterpret_cast<const char*>(packed);
     const int H = (int)(D / kHeadDim);
 
-    hipError_t e = launch_embed(T, D, R, V, tokens, req_offsets, emb, x, pos, offs, s);
-    if (e == hipSuccess) e = launch_rms_to_bf16(T, D, x, offs, 1, rms_eps, a, s);
-    if (e == hipSuccess)
-        e = launch_grouped_gemm(false, EPI_STORE, plain_args(a, D, pk, 3 * D, offs, T, qkv, 3 * D),
-                                s);
+    // Tiles of the four GEMMs (K = D): measured on MI355X at Table 1's widths
+    // over 8192 tokens, where the automatic choice (tuned for the experts'
+    // K of 4096 - 8192) leaves most CUs idle on the N = D products.
+    const bool wide = T >= 2048 && D <= 1024;
+    hipError_t e = launch_embed_norm(T, D, R, V, rms_eps, tokens, req_offsets, emb, x, a, pos,
+                                     offs, s);
+    if (e == hipSuccess) {
+        GemmArgs g = plain_args(a, D, pk, 3 * D, offs, T, qkv, 3 * D);
+        g.tile = wide ? kTileQkv : 0;
+        e = launch_grouped_gemm(false, EPI_STORE, g, s);
+    }
     if (e == hipSuccess) e = launch_rope(T, 2 * H, pos, qkv, 3 * D, s);
     if (e == hipSuccess)
         e = launch_attention(T, H, pos, qkv, qkv + D, qkv + 2 * D, 3 * D, o, D, s);
-    if (e == hipSuccess)
-        e = launch_grouped_gemm(false, EPI_RESID_ADD,
-                                plain_args(o, D, pk + 3 * D * D * 2, D, offs, T, x, D), s);
-    if (e == hipSuccess) e = launch_rms_to_bf16(T, D, x, offs, 1, rms_eps, m, s);
+    if (e == hipSuccess) {
+        GemmArgs g = plain_args(o, D, pk + 3 * D * D * 2, D, offs, T, x, D);
+        g.tile = wide ? kTileNarrow : 0;
+        e = launch_grouped_gemm(false, EPI_RESID_ADD, g, s);
+    }
+    if (e == hipSuccess) e = launch_rms_rows(T, D, rms_eps, x, m, s);
     const void* mlp = pk + 4 * D * D * 2;
     if (e == hipSuccess) {
         GemmArgs gu = gate_up_args(README_BF16, T, D, 1, F, m, offs, mlp, h);
         gu.m_tiles32 = (int)ceil_div(T, 32);
+        gu.tile = wide ? kTileGateUp : 0;
         e = launch_grouped_gemm(false, EPI_GATE_UP_SILU, gu, s);
     }
     if (e == hipSuccess) {
         GemmArgs dn = down_args(README_BF16, T, D, 1, F, h, offs, mlp, x);
         dn.m_tiles32 = (int)ceil_div(T, 32);
+        dn.tile = wide ? kTileNarrow : 0;
         e = launch_grouped_gemm(false, EPI_RESID_ADD, dn, s);
     }
-    if (e == hipSuccess) e = launch_rms_to_bf16(T, D, x, offs, 1, rms_eps, feat, s);
     if (e == hipSuccess)
-        e = launch_route(README_BF16, T, D, E, feat, w_router, bias, expert_ids, logits, s);
+        e = launch_norm_gate(T, D, E, rms_eps, x, w_router, bias, feat, expert_ids, logits, s);
     return st_of(e);
 }
 

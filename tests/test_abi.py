@@ -228,6 +228,8 @@ def test_router_tf_sizes_and_errors(lib):
     assert at(0, 2, None, None, None, None, 256, None, 256, None) == 0
     ro = lib.readme_rope
     assert ro(10, 2, FAKE, FAKE, 255, None) == 1
+    assert ro(10, 2, FAKE, FAKE, 260, None) == 1                             # ld % 8
+    assert ro(10, 2, FAKE, ctypes.c_void_p(4104), 256, None) == 1            # misaligned
     assert ro(0, 2, None, None, 256, None) == 0
     rp = lib.readme_request_positions
     assert rp(10, 0, FAKE, FAKE, None) == 1
