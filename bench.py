@@ -363,14 +363,14 @@ TRAFFIC = {
     # profiles/traffic_gate_up_prefill_skew16.md), or the whole 32-layer stack
     # (profiles/traffic_stack_llama7b_decode32.md)
     "wide_requests": (_GEMM_SOURCES,
-                      "d4951901d248354cb44ddbec258d61f67ce545529dedb524aa5105a139737687",
-                      2257194574, 58720256),
+                      "f2e5982ee17904e80e59c9f86a5a9dcabc2500a967656b365c81d094c306a252",
+                      2255728392, 58720256),
     "prefill_skew16": (_GEMM_SOURCES,
-                       "d4951901d248354cb44ddbec258d61f67ce545529dedb524aa5105a139737687",
-                       609878110, 23068672),
+                       "f2e5982ee17904e80e59c9f86a5a9dcabc2500a967656b365c81d094c306a252",
+                       609159683, 23068672),
     "llama7b_decode32": (_STACK_SOURCES,
-                         "be1919bf82f2577568b294126229d686c2514bd08643daebe94322fb15a5c4cd",
-                         7874061121, 56098816),
+                         "a756ab735425f3c3076cc6ab0098e362b9a17ea201cdde28fde69a3b168da6ea",
+                         7874059189, 56098816),
 }
 
 
