@@ -665,16 +665,24 @@ def router_flops(shape: wl.RouterShape, lengths) -> float:
     return T * (8.0 * D * D + 6.0 * D * F + 2.0 * D * E) + 4.0 * 128 * prefix * (D // 128)
 
 
-def router_line(K: int, W: int) -> dict:
+ROUTER_MIXES = {
+    # name: request lengths (8192 tokens each)
+    "requests_256x32": [32] * 256,     # the request batch's requests
+    "prompts_8x1024": [1024] * 8,      # long prompts: attention over 1024-token prefixes
+}
+
+
+def router_line(K: int, W: int, mix: str = "requests_256x32") -> dict:
     """The pre-gating router G (Sec. 2.3, Table 1: one causal transformer
     block of width 512, four heads, SwiGLU MLP 512, vocabulary 32000, then
-    the gate to 8 experts) over the request batch's tokens, 256 requests x
-    32 tokens, random-init weights.  One call = embedding, block, gate, all
-    on the GPU; HIP events on the launch stream around K calls."""
+    the gate to 8 experts) over 8192 tokens in requests of the given mix
+    (by default the request batch's 256 x 32), random-init weights.  One
+    call = embedding, block, gate, all on the GPU; HIP events on the launch
+    stream around K calls."""
     import torch
     from paper_2410_19123_amd import _lib as L
     shape = wl.ROUTER_TABLE1
-    lengths = [32] * 256
+    lengths = ROUTER_MIXES[mix]
     wts = wl.make_router_tf(shape, 0)
     tokens, ro = wl.make_router_requests(lengths, shape.V, 0)
     dev = torch.device("cuda:0")
@@ -705,7 +713,7 @@ def router_line(K: int, W: int) -> dict:
     us = t0.elapsed_time(t1) * 1e3 / K
     fl = router_flops(shape, lengths)
     counts = np.bincount(L.from_device(ids), minlength=shape.E)
-    out = {"workload": "router_tf_table1_requests_256x32", "T": T, "D": shape.D, "F": shape.F,
+    out = {"workload": f"router_tf_table1_{mix}", "T": T, "D": shape.D, "F": shape.F,
            "V": shape.V, "E": shape.E, "heads": shape.D // 128, "requests": len(lengths),
            "steps": K, "us_per_call": round(us, 2), "tokens_per_s": round(T / (us * 1e-6), 1),
            "gflop_per_call": round(fl / 1e9, 3), "tflops": round(fl / (us * 1e-6) / 1e12, 2),
@@ -728,7 +736,9 @@ def main():
         sys.exit(1)
 
     if args.router_only:
-        print(json.dumps({"router": router_line(args.steps, args.warmup)}), flush=True)
+        print(json.dumps({"router": router_line(args.steps, args.warmup),
+                          "router_long": router_line(args.steps, args.warmup,
+                                                     "prompts_8x1024")}), flush=True)
         return
 
     w = wl.WORKLOADS[args.workload]

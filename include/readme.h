@@ -747,10 +747,14 @@ readme_status readme_rope(int64_t T, int32_t H, const int32_t *pos, void *x, int
  * (hi + lo, about 16 significant bits), so o is the exact result up to
  * about 2^-16 of the largest |v| plus the final bf16 rounding.
  *   q, k, v  [T][ld_in] bf16 (head h at columns 128h ..), o [T][ld_out] bf16
- *   out, pos [T] int32.  Requires ld_in, ld_out >= 128 H and multiples of 8,
- *   16-byte aligned q, k, v, o, H <= 65535.  o must not overlap q, k or v.
+ *   out, pos [T] int32.  R, the number of requests the tokens form, only
+ *   picks the launch shape (from a mean of 128 tokens per request, four
+ *   waves per workgroup share each key block; below, one wave loops over
+ *   its own queries' blocks): every R >= 0 gives the same bits.  Requires
+ *   ld_in, ld_out >= 128 H and multiples of 8, 16-byte aligned q, k, v, o,
+ *   H <= 65535.  o must not overlap q, k or v.
  */
-readme_status readme_attention_causal(int64_t T, int32_t H, const int32_t *pos,
+readme_status readme_attention_causal(int64_t T, int32_t H, int32_t R, const int32_t *pos,
                                       const void *q, const void *k, const void *v,
                                       int64_t ld_in, void *o, int64_t ld_out, void *stream);
 

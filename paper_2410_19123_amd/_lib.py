@@ -90,7 +90,7 @@ SIGNATURES = {
                                 _P, _P, _P, _SZ, _P]),
     "readme_request_positions": (_I32, [_I64, _I32, _P, _P, _P]),
     "readme_rope": (_I32, [_I64, _I32, _P, _P, _I64, _P]),
-    "readme_attention_causal": (_I32, [_I64, _I32, _P, _P, _P, _P, _I64, _P, _I64, _P]),
+    "readme_attention_causal": (_I32, [_I64, _I32, _I32, _P, _P, _P, _P, _I64, _P, _I64, _P]),
 }
 
 # Workspace regions of readme_router_tf (README_RTF_*).
@@ -744,16 +744,17 @@ def readme_rope(x, pos, H: int):
     return x
 
 
-def readme_attention_causal(q, k, v, pos, H: int, o=None):
-    """Causal attention inside each request (bf16 [T][ld], heads of 128)."""
+def readme_attention_causal(q, k, v, pos, H: int, R: int = 1, o=None):
+    """Causal attention inside each request (bf16 [T][ld], heads of 128);
+    R (the number of requests) only picks the launch shape."""
     T, ld = q.shape
     if k.shape != q.shape or v.shape != q.shape:
         raise ValueError("q, k, v shapes disagree")
     if o is None:
         o = torch.empty(T, H * 128, dtype=torch.bfloat16, device=q.device)
     _dev(q, k, v, pos, o)
-    _call("readme_attention_causal", T, H, _p(pos), _p(q), _p(k), _p(v), ld, _p(o), o.shape[1],
-          _stream(q.device))
+    _call("readme_attention_causal", T, H, R, _p(pos), _p(q), _p(k), _p(v), ld, _p(o),
+          o.shape[1], _stream(q.device))
     return o
 
 

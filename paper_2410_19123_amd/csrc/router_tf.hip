@@ -30,11 +30,12 @@ namespace {
 constexpr int kHeadDim = 128;
 // log2(e) / sqrt(128): scores go to exp2 in one multiply.
 constexpr float kScoreScale = 0.12751743082459868f;
-// Waves (of 32 queries each) per attention workgroup: one, so that a wave
-// loops only over its own queries' key blocks (a request batch of short
-// requests then needs one key block per wave) and no wave waits at another's
-// barrier.
-constexpr int kAttnWaves = 1;
+// Mean request length from which attention runs four waves per workgroup
+// sharing each key block (below it, one wave per workgroup loops only over
+// its own queries' blocks: a request batch of short requests then needs one
+// key block per wave and no wave waits at another's barrier).
+constexpr int kAttnLongMean = 128;
+constexpr int kAttnLongWaves = 4;
 
 // First token of t's request, from the in-request position (clamped, so a
 // malformed position never leads outside [0, t]).
@@ -327,8 +328,10 @@ __global__ __launch_bounds__(256) void k_rope(int64_t T, int NH,
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-// Causal attention of one 128-dim head over 128 queries per workgroup.
+// Causal attention of one 128-dim head over 32 * NW queries per workgroup.
 //   Wave w owns queries t = q0 + 32w + (lane % 32); both half-waves hold the
 //   same queries (the matrix-core layout splits each key block between
 //   them).  Per key block of 32 rows, staged in LDS (K row-major, V
@@ -345,6 +348,11 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 //   o = O / l, rounded to bf16.  Key blocks run from the first query's
 //   request start to the last query; a wave skips the blocks outside its own
 //   queries' range (the workgroup still passes every barrier).
+//   NW = 1 (short requests): each wave loads only its own blocks, one LDS
+//   buffer.  NW = 4 (long requests): the four waves share each block, two
+//   LDS buffers, and block kb+1 is requested into registers before block kb
+//   is computed and written to the other buffer after it, one barrier per
+//   block.
 template <int NW>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void k_attention_causal(int64_t T, const int32_t* __restrict__ pos,
@@ -353,8 +361,11 @@ void k_attention_causal(int64_t T, const int32_t* __restrict__ pos,
                         int64_t ldo) {
     constexpr int KP = kHeadDim + 8;  // K rows in LDS, 272 bytes apart
     constexpr int VP = 32 + 8;        // V^T rows (one per dim), 80 bytes apart
-    __shared__ __attribute__((aligned(16))) uint16_t k_lds[32 * KP];
-    __shared__ __attribute__((aligned(16))) uint16_t vt_lds[kHeadDim * VP];
+    constexpr bool PF = NW > 1;       // next block in flight during this one
+    constexpr int NB = PF ? 2 : 1;    // LDS buffers
+    constexpr int NCH = 32 * (kHeadDim / 8) / (64 * NW);  // 16-byte chunks per thread
+    __shared__ __attribute__((aligned(16))) uint16_t k_lds[NB][32 * KP];
+    __shared__ __attribute__((aligned(16))) uint16_t vt_lds[NB][kHeadDim * VP];
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int hf = lane >> 5, col = lane & 31;
@@ -371,6 +382,36 @@ void k_attention_causal(int64_t T, const int32_t* __restrict__ pos,
     const int64_t lo = request_start(q0, pos);
     const int64_t hi = q0 + 32 * NW - 1 < T - 1 ? q0 + 32 * NW - 1 : T - 1;
 
+    // Chunk i of this thread: key row c / 16, 8 dims at 8 * (c % 16).
+    uint4 kr[NCH], vr[NCH];
+    auto fetch = [&](int64_t kb) {
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+            const int c = tid + i * 64 * NW;
+            const int64_t key = kb * 32 + (c >> 4);
+            kr[i] = make_uint4(0u, 0u, 0u, 0u);
+            vr[i] = kr[i];
+            if (key < T) {
+                kr[i] = *reinterpret_cast<const uint4*>(k + key * ldi + hoff + (c & 15) * 8);
+                vr[i] = *reinterpret_cast<const uint4*>(v + key * ldi + hoff + (c & 15) * 8);
+            }
+        }
+    };
+    auto stash = [&](int b) {
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+            const int c = tid + i * 64 * NW;
+            const int r = c >> 4, ch = c & 15;
+            *reinterpret_cast<uint4*>(&k_lds[b][r * KP + ch * 8]) = kr[i];
+            const uint32_t vw[4] = {vr[i].x, vr[i].y, vr[i].z, vr[i].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                vt_lds[b][(ch * 8 + 2 * e) * VP + r] = (uint16_t)(vw[e] & 0xffffu);
+                vt_lds[b][(ch * 8 + 2 * e + 1) * VP + r] = (uint16_t)(vw[e] >> 16);
+            }
+        }
+    };
+
     bf16x8 qf[8];
     {
         const uint16_t* qrow = q + tq * ldi + hoff + hf * 8;
@@ -384,87 +425,96 @@ void k_attention_causal(int64_t T, const int32_t* __restrict__ pos,
         for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
     float m_run = -INFINITY, l_run = 0.0f;
 
-    for (int64_t kb = lo >> 5; kb <= (hi >> 5); ++kb) {
+    auto compute = [&](int64_t kb, int b) {
         const int64_t k0 = kb * 32;
-        for (int c = tid; c < 32 * (kHeadDim / 8); c += 64 * NW) {
-            const int r = c >> 4, ch = c & 15;
-            const int64_t key = k0 + r;
-            uint4 kv = make_uint4(0u, 0u, 0u, 0u), vv = kv;
-            if (key < T) {
-                kv = *reinterpret_cast<const uint4*>(k + key * ldi + hoff + ch * 8);
-                vv = *reinterpret_cast<const uint4*>(v + key * ldi + hoff + ch * 8);
-            }
-            *reinterpret_cast<uint4*>(k_lds + r * KP + ch * 8) = kv;
-            const uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
+        if (!(wact && k0 <= whi && k0 + 31 >= wlo)) return;
+        f32x16 s;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                vt_lds[(ch * 8 + 2 * e) * VP + r] = (uint16_t)(vw[e] & 0xffffu);
-                vt_lds[(ch * 8 + 2 * e + 1) * VP + r] = (uint16_t)(vw[e] >> 16);
-            }
+        for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) {
+            const bf16x8 kf =
+                *reinterpret_cast<const bf16x8*>(&k_lds[b][col * KP + ks * 16 + hf * 8]);
+            s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s, 0, 0, 0);
         }
-        __syncthreads();
-        if (wact && k0 <= whi && k0 + 31 >= wlo) {
-            f32x16 s;
+        // lane holds keys k0 + 4*hf + off(r), off(r) = 8*(r/4) + (r%4), of
+        // query t; the key is valid for lo_off <= off(r) <= hi_off
+        const int lo_off = (int)(start - k0) - 4 * hf;
+        const int hi_off = tv ? (int)(t - k0) - 4 * hf : -1;
+        float sv[16];
+        float mb = -INFINITY;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+        for (int r = 0; r < 16; ++r) {
+            const int off = 8 * (r >> 2) + (r & 3);
+            sv[r] = ((off >= lo_off) & (off <= hi_off)) ? s[r] * kScoreScale : -INFINITY;
+            mb = fmaxf(mb, sv[r]);
+        }
+        mb = fmaxf(mb, __shfl_xor(mb, 32, 64));
+        const float mn = fmaxf(m_run, mb);
+        const float base = mn == -INFINITY ? 0.0f : mn;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - base);
+        m_run = mn;
+        l_run *= alpha;
+        // The weights' hi and lo bf16 parts, two per instruction (the
+        // matrix-core conversion rounds to nearest even; p is finite)
+        uint32_t ph[8], pl[8];
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks) {
-                const bf16x8 kf =
-                    *reinterpret_cast<const bf16x8*>(k_lds + col * KP + ks * 16 + hf * 8);
-                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s, 0, 0, 0);
-            }
-            // lane holds keys k0 + 8*(r/4) + 4*hf + (r%4) of query t
-            float sv[16];
-            float mb = -INFINITY;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int64_t key = k0 + 8 * (r >> 2) + 4 * hf + (r & 3);
-                const bool ok = tv && key >= start && key <= t;
-                sv[r] = ok ? s[r] * kScoreScale : -INFINITY;
-                mb = fmaxf(mb, sv[r]);
-            }
-            mb = fmaxf(mb, __shfl_xor(mb, 32, 64));
-            const float mn = fmaxf(m_run, mb);
-            const float base = mn == -INFINITY ? 0.0f : mn;
-            const float alpha = exp2f(m_run - base);
-            m_run = mn;
-            l_run *= alpha;
-            uint32_t ph[8], pl[8];
-#pragma unroll
-            for (int r = 0; r < 16; r += 2) {
-                const float p0 = exp2f(sv[r] - base), p1 = exp2f(sv[r + 1] - base);
-                l_run += p0;
-                l_run += p1;
-                const uint16_t h0 = f32_to_bf16(p0), h1 = f32_to_bf16(p1);
-                const uint16_t e0 = f32_to_bf16(p0 - bf16_lo(h0));
-                const uint16_t e1 = f32_to_bf16(p1 - bf16_lo(h1));
-                ph[r >> 1] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-                pl[r >> 1] = (uint32_t)e0 | ((uint32_t)e1 << 16);
-            }
+        for (int r = 0; r < 16; r += 2) {
+            const f32x2 p = {__builtin_amdgcn_exp2f(sv[r] - base),
+                             __builtin_amdgcn_exp2f(sv[r + 1] - base)};
+            l_run += p[0];
+            l_run += p[1];
+            const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(p, bf16x2));
+            const f32x2 e = {p[0] - bf16_lo(h), p[1] - bf16_hi(h)};
+            ph[r >> 1] = h;
+            pl[r >> 1] = __builtin_bit_cast(uint32_t, __builtin_convertvector(e, bf16x2));
+        }
+        if (__any(alpha != 1.0f)) {  // a factor of exactly 1 changes nothing
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[mt][r] *= alpha;
+        }
 #pragma unroll
-            for (int kk = 0; kk < 2; ++kk) {
-                const u32x4 bh = {ph[4 * kk], ph[4 * kk + 1], ph[4 * kk + 2], ph[4 * kk + 3]};
-                const u32x4 bl = {pl[4 * kk], pl[4 * kk + 1], pl[4 * kk + 2], pl[4 * kk + 3]};
+        for (int kk = 0; kk < 2; ++kk) {
+            const u32x4 bh = {ph[4 * kk], ph[4 * kk + 1], ph[4 * kk + 2], ph[4 * kk + 3]};
+            const u32x4 bl = {pl[4 * kk], pl[4 * kk + 1], pl[4 * kk + 2], pl[4 * kk + 3]};
 #pragma unroll
-                for (int mt = 0; mt < 4; ++mt) {
-                    const uint16_t* vr = vt_lds + (mt * 32 + col) * VP + 16 * kk + 4 * hf;
-                    const uint2 a0 = *reinterpret_cast<const uint2*>(vr);
-                    const uint2 a1 = *reinterpret_cast<const uint2*>(vr + 8);
-                    const u32x4 av = {a0.x, a0.y, a1.x, a1.y};
-                    acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8, av), __builtin_bit_cast(bf16x8, bh), acc[mt],
-                        0, 0, 0);
-                    acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        __builtin_bit_cast(bf16x8, av), __builtin_bit_cast(bf16x8, bl), acc[mt],
-                        0, 0, 0);
-                }
+            for (int mt = 0; mt < 4; ++mt) {
+                const uint16_t* vp = &vt_lds[b][(mt * 32 + col) * VP + 16 * kk + 4 * hf];
+                const uint2 a0 = *reinterpret_cast<const uint2*>(vp);
+                const uint2 a1 = *reinterpret_cast<const uint2*>(vp + 8);
+                const u32x4 av = {a0.x, a0.y, a1.x, a1.y};
+                acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8, av), __builtin_bit_cast(bf16x8, bh), acc[mt], 0,
+                    0, 0);
+                acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8, av), __builtin_bit_cast(bf16x8, bl), acc[mt], 0,
+                    0, 0);
             }
         }
+    };
+
+    const int64_t kb0 = lo >> 5, kb1 = hi >> 5;
+    if constexpr (PF) {
+        fetch(kb0);
+        stash((int)(kb0 & 1));
         __syncthreads();
+        for (int64_t kb = kb0; kb <= kb1; ++kb) {
+            const int b = (int)(kb & 1);
+            if (kb < kb1) fetch(kb + 1);
+            compute(kb, b);
+            if (kb < kb1) stash(b ^ 1);
+            __syncthreads();
+        }
+    } else {
+        for (int64_t kb = kb0; kb <= kb1; ++kb) {
+            fetch(kb);
+            stash(0);
+            __syncthreads();
+            compute(kb, 0);
+            __syncthreads();
+        }
     }
 
     const float lt = l_run + __shfl_xor(l_run, 32, 64);
@@ -540,12 +590,23 @@ hipError_t launch_rope(int64_t T, int NH, const int32_t* pos, void* x, int64_t l
     return hipGetLastError();
 }
 
-hipError_t launch_attention(int64_t T, int H, const int32_t* pos, const void* q, const void* k,
-                            const void* v, int64_t ldi, void* o, int64_t ldo, hipStream_t s) {
-    const dim3 grid((unsigned)ceil_div(T, 32 * kAttnWaves), (unsigned)H);
-    k_attention_causal<kAttnWaves><<<grid, 64 * kAttnWaves, 0, s>>>(
-        T, pos, reinterpret_cast<const uint16_t*>(q), reinterpret_cast<const uint16_t*>(k),
-        reinterpret_cast<const uint16_t*>(v), ldi, reinterpret_cast<uint16_t*>(o), ldo);
+// Requests of 128 tokens or more on average take the four-wave pipelined
+// form (the waves share each key block); shorter ones the single-wave form.
+hipError_t launch_attention(int64_t T, int H, int32_t R, const int32_t* pos, const void* q,
+                            const void* k, const void* v, int64_t ldi, void* o, int64_t ldo,
+                            hipStream_t s) {
+    const auto* qb = reinterpret_cast<const uint16_t*>(q);
+    const auto* kb = reinterpret_cast<const uint16_t*>(k);
+    const auto* vb = reinterpret_cast<const uint16_t*>(v);
+    auto* ob = reinterpret_cast<uint16_t*>(o);
+    if (T >= (int64_t)kAttnLongMean * (R > 0 ? R : 1)) {
+        const dim3 grid((unsigned)ceil_div(T, 32 * kAttnLongWaves), (unsigned)H);
+        k_attention_causal<kAttnLongWaves><<<grid, 64 * kAttnLongWaves, 0, s>>>(
+            T, pos, qb, kb, vb, ldi, ob, ldo);
+    } else {
+        const dim3 grid((unsigned)ceil_div(T, 32), (unsigned)H);
+        k_attention_causal<1><<<grid, 64, 0, s>>>(T, pos, qb, kb, vb, ldi, ob, ldo);
+    }
     return hipGetLastError();
 }
 
@@ -672,17 +733,17 @@ readme_status readme_rope(int64_t T, int32_t H, const int32_t* pos, void* x, int
     return st_of(launch_rope(T, H, pos, x, ld, as_stream(stream)));
 }
 
-readme_status readme_attention_causal(int64_t T, int32_t H, const int32_t* pos, const void* q,
-                                      const void* k, const void* v, int64_t ld_in, void* o,
-                                      int64_t ld_out, void* stream) {
-    if (T < 0 || H < 0) return README_ERR_ARG;
+readme_status readme_attention_causal(int64_t T, int32_t H, int32_t R, const int32_t* pos,
+                                      const void* q, const void* k, const void* v, int64_t ld_in,
+                                      void* o, int64_t ld_out, void* stream) {
+    if (T < 0 || H < 0 || R < 0) return README_ERR_ARG;
     if (ld_in < (int64_t)H * kHeadDim || ld_out < (int64_t)H * kHeadDim) return README_ERR_ARG;
     if (T > INT32_MAX || H > 65535) return README_ERR_UNSUPPORTED;
     if (T == 0 || H == 0) return README_OK;
     if (!pos || !q || !k || !v || !o) return README_ERR_ARG;
     if (!al16(q) || !al16(k) || !al16(v) || !al16(o) || ld_in % 8 || ld_out % 8)
         return README_ERR_ARG;
-    return st_of(launch_attention(T, H, pos, q, k, v, ld_in, o, ld_out, as_stream(stream)));
+    return st_of(launch_attention(T, H, R, pos, q, k, v, ld_in, o, ld_out, as_stream(stream)));
 }
 
 readme_status readme_router_tf(int64_t T, int32_t R, int64_t D, int64_t F, int32_t E, int64_t V,
@@ -730,7 +791,7 @@ readme_status readme_router_tf(int64_t T, int32_t R, int64_t D, int64_t F, int32
     }
     if (e == hipSuccess) e = launch_rope(T, 2 * H, pos, qkv, 3 * D, s);
     if (e == hipSuccess)
-        e = launch_attention(T, H, pos, qkv, qkv + D, qkv + 2 * D, 3 * D, o, D, s);
+        e = launch_attention(T, H, R, pos, qkv, qkv + D, qkv + 2 * D, 3 * D, o, D, s);
     if (e == hipSuccess) {
         GemmArgs g = plain_args(o, D, pk + 3 * D * D * 2, D, offs, T, x, D);
         g.tile = wide ? kTileNarrow : 0;

@@ -222,10 +222,11 @@ def test_router_tf_sizes_and_errors(lib):
     assert pk(512, 512, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == 1
     assert pk(640, 0, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == 1
     at = lib.readme_attention_causal
-    assert at(10, 2, FAKE, FAKE, FAKE, FAKE, 200, FAKE, 256, None) == 1      # ld_in < 256
-    assert at(10, 2, FAKE, FAKE, FAKE, FAKE, 260, FAKE, 256, None) == 1      # ld_in % 8
-    assert at(10, 2, FAKE, ctypes.c_void_p(4104), FAKE, FAKE, 256, FAKE, 256, None) == 1
-    assert at(0, 2, None, None, None, None, 256, None, 256, None) == 0
+    assert at(10, 2, 1, FAKE, FAKE, FAKE, FAKE, 200, FAKE, 256, None) == 1   # ld_in < 256
+    assert at(10, 2, 1, FAKE, FAKE, FAKE, FAKE, 260, FAKE, 256, None) == 1   # ld_in % 8
+    assert at(10, 2, 1, FAKE, ctypes.c_void_p(4104), FAKE, FAKE, 256, FAKE, 256, None) == 1
+    assert at(10, 2, -1, FAKE, FAKE, FAKE, FAKE, 256, FAKE, 256, None) == 1  # R < 0
+    assert at(0, 2, 0, None, None, None, None, 256, None, 256, None) == 0
     ro = lib.readme_rope
     assert ro(10, 2, FAKE, FAKE, 255, None) == 1
     assert ro(10, 2, FAKE, FAKE, 260, None) == 1                             # ld % 8

@@ -118,15 +118,21 @@ def test_rope_bit_exact(T, H, ld, maxpos):
     assert np.array_equal(got, ref), f"{int((got != ref).sum())} elements differ"
 
 
-@pytest.mark.parametrize("lengths,H,scale", [
+ATTN_CASES = [
     ([1], 1, 1.0),
     ([37], 2, 1.0),
     ([32, 32, 32, 32, 32], 1, 2.0),
     ([0, 1, 31, 33, 0, 127, 128, 129, 5], 2, 1.5),
     ([600], 1, 3.0),
     ([300, 45, 0, 211, 1, 1], 4, 1.0),
-])
+    ([1000, 3, 700], 2, 2.0),
+]
+
+
+@pytest.mark.parametrize("lengths,H,scale", ATTN_CASES)
 def test_attention_matches_oracle(lengths, H, scale):
+    """Both launch shapes (one wave per workgroup, and four sharing each key
+    block with the next block in flight) on every case; the same bits."""
     L = _lib()
     ro = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
     T = int(ro[-1])
@@ -134,8 +140,11 @@ def test_attention_matches_oracle(lengths, H, scale):
     q, k, v = (wl.to_bf16_bits(rng.standard_normal((T, H * HD)).astype(np.float32) * s)
                for s in (scale, scale, 1.0))
     pos = R.positions(ro, T).astype(np.int32)
-    got = from_dev(L.readme_attention_causal(to_dev(q), to_dev(k), to_dev(v), to_dev(pos), H))
-    _attention_ok(got, q, k, v, ro, f"attention {lengths} H={H}")
+    dq, dk, dv, dp = to_dev(q), to_dev(k), to_dev(v), to_dev(pos)
+    short = from_dev(L.readme_attention_causal(dq, dk, dv, dp, H, R=max(T, 1)))
+    long_ = from_dev(L.readme_attention_causal(dq, dk, dv, dp, H, R=1))
+    _attention_ok(short, q, k, v, ro, f"attention {lengths} H={H}, one wave")
+    assert np.array_equal(short, long_), "launch shapes differ"
 
 
 def _forward(shape, lengths, seed):
