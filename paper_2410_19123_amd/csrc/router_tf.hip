@@ -77,10 +77,14 @@ __device__ __forceinline__ float wave_sum_bcast(float v) {
 // workgroup): x[t] = fp32(emb[tokens[t]]) (zeros for an id outside [0, V)),
 // a[t] = bf16(x[t] * r), r = 1 / sqrt(mean x^2 + eps) in fp32 (each lane sums
 // its elements in ascending order, then the wave folds).  Lane l owns the
-// 8-element chunks l, l + 64, ...; the row is read once more from the
-// (cached) table for the second pass.  Lane 0 writes pos[t], found by binary
-// search over the request offsets (staged in LDS when R + 1 <= 4096);
-// thread 0 of block 0 writes the offsets {0, T} of the one-group GEMMs.
+// 8-element chunks l, l + 64, ...: NC > 0 of them (D <= 512 NC) held in
+// registers, or with NC = 0 any number, the row read once more from the
+// (cached) table for the second pass.  The token id is read before the
+// workgroup's barrier, so its round trip overlaps the staging of the request
+// offsets in LDS (when R + 1 <= 4096) that the position search of lane 0
+// reads; thread 0 of block 0 writes the offsets {0, T} of the one-group
+// GEMMs.
+template <int NC>
 __global__ __launch_bounds__(256) void k_embed_norm(int64_t T, int64_t D, int32_t R, int64_t V,
                                                     float eps,
                                                     const int32_t* __restrict__ tokens,
@@ -91,6 +95,9 @@ __global__ __launch_bounds__(256) void k_embed_norm(int64_t T, int64_t D, int32_
                                                     int32_t* __restrict__ pos,
                                                     int32_t* __restrict__ offs) {
     __shared__ int32_t ro_lds[kRoLds];
+    const int lane = threadIdx.x & 63;
+    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t tok = t < T ? (int64_t)tokens[t] : -1;
     const bool staged = R + 1 <= kRoLds;
     if (staged)
         for (int i = threadIdx.x; i <= R; i += blockDim.x) ro_lds[i] = ro[i];
@@ -99,18 +106,16 @@ __global__ __launch_bounds__(256) void k_embed_norm(int64_t T, int64_t D, int32_
         offs[1] = (int32_t)T;
     }
     __syncthreads();
-    const int lane = threadIdx.x & 63;
-    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (t >= T) return;
-    if (lane == 0) pos[t] = position_of(t, R, staged ? ro_lds : ro);
-    const int64_t tok = tokens[t];
     const bool ok = tok >= 0 && tok < V;
     const uint16_t* er = emb + (ok ? tok : 0) * D;
     const int64_t nch = D / 8;
-    float ss = 0.0f;
-    for (int64_t c = lane; c < nch; c += 64) {
+    auto load = [&](int64_t c) {
         uint4 w = make_uint4(0u, 0u, 0u, 0u);
         if (ok) w = *reinterpret_cast<const uint4*>(er + c * 8);
+        return w;
+    };
+    auto put_x = [&](int64_t c, const uint4 w, float& ss) {
         const float v[8] = {bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y),
                             bf16_lo(w.z), bf16_hi(w.z), bf16_lo(w.w), bf16_hi(w.w)};
         float4* dst = reinterpret_cast<float4*>(x + t * D + c * 8);
@@ -118,17 +123,34 @@ __global__ __launch_bounds__(256) void k_embed_norm(int64_t T, int64_t D, int32_
         dst[1] = make_float4(v[4], v[5], v[6], v[7]);
 #pragma unroll
         for (int k = 0; k < 8; ++k) ss += v[k] * v[k];
-    }
-    const float r = 1.0f / sqrtf(wave_sum_bcast(ss) / (float)D + eps);
-    for (int64_t c = lane; c < nch; c += 64) {
-        uint4 w = make_uint4(0u, 0u, 0u, 0u);
-        if (ok) w = *reinterpret_cast<const uint4*>(er + c * 8);
+    };
+    auto put_a = [&](int64_t c, const uint4 w, float r) {
         uint4 o;
         o.x = (uint32_t)f32_to_bf16(bf16_lo(w.x) * r) | ((uint32_t)f32_to_bf16(bf16_hi(w.x) * r) << 16);
         o.y = (uint32_t)f32_to_bf16(bf16_lo(w.y) * r) | ((uint32_t)f32_to_bf16(bf16_hi(w.y) * r) << 16);
         o.z = (uint32_t)f32_to_bf16(bf16_lo(w.z) * r) | ((uint32_t)f32_to_bf16(bf16_hi(w.z) * r) << 16);
         o.w = (uint32_t)f32_to_bf16(bf16_lo(w.w) * r) | ((uint32_t)f32_to_bf16(bf16_hi(w.w) * r) << 16);
         *reinterpret_cast<uint4*>(a + t * D + c * 8) = o;
+    };
+    float ss = 0.0f;
+    if constexpr (NC > 0) {
+        uint4 w[NC];
+#pragma unroll
+        for (int j = 0; j < NC; ++j)
+            if (lane + 64 * j < nch) w[j] = load(lane + 64 * j);
+        if (lane == 0) pos[t] = position_of(t, R, staged ? ro_lds : ro);
+#pragma unroll
+        for (int j = 0; j < NC; ++j)
+            if (lane + 64 * j < nch) put_x(lane + 64 * j, w[j], ss);
+        const float r = 1.0f / sqrtf(wave_sum_bcast(ss) / (float)D + eps);
+#pragma unroll
+        for (int j = 0; j < NC; ++j)
+            if (lane + 64 * j < nch) put_a(lane + 64 * j, w[j], r);
+    } else {
+        if (lane == 0) pos[t] = position_of(t, R, staged ? ro_lds : ro);
+        for (int64_t c = lane; c < nch; c += 64) put_x(c, load(c), ss);
+        const float r = 1.0f / sqrtf(wave_sum_bcast(ss) / (float)D + eps);
+        for (int64_t c = lane; c < nch; c += 64) put_a(c, load(c), r);
     }
 }
 
@@ -183,6 +205,18 @@ __global__ __launch_bounds__(256) void k_norm_gate(int64_t T, int64_t D, int E, 
     const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (t >= T) return;
     const int nch = (int)(D / 8);
+    // The first eight experts' gate rows are requested with x, so that their
+    // round trip overlaps the norm.
+    uint4 w0[8][NC];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int e = i < E ? i : E - 1;
+#pragma unroll
+        for (int j = 0; j < NC; ++j) {
+            const int c = lane + 64 * j;
+            if (c < nch) w0[i][j] = *reinterpret_cast<const uint4*>(w + (int64_t)e * D + (int64_t)c * 8);
+        }
+    }
     float v[NC][8];
     float ss = 0.0f;
 #pragma unroll
@@ -232,7 +266,8 @@ __global__ __launch_bounds__(256) void k_norm_gate(int64_t T, int64_t D, int E, 
                 const int c = lane + 64 * j;
                 if (c < nch) {
                     const uint4 wv =
-                        *reinterpret_cast<const uint4*>(w + (int64_t)e * D + (int64_t)c * 8);
+                        e0 == 0 ? w0[i][j]
+                                : *reinterpret_cast<const uint4*>(w + (int64_t)e * D + (int64_t)c * 8);
                     const float wf[8] = {bf16_lo(wv.x), bf16_hi(wv.x), bf16_lo(wv.y),
                                          bf16_hi(wv.y), bf16_lo(wv.z), bf16_hi(wv.z),
                                          bf16_lo(wv.w), bf16_hi(wv.w)};
@@ -545,8 +580,16 @@ hipError_t launch_embed_norm(int64_t T, int64_t D, int32_t R, int64_t V, float e
                              const int32_t* tokens, const int32_t* ro, const void* emb,
                              float* x, uint16_t* a, int32_t* pos, int32_t* offs,
                              hipStream_t s) {
-    k_embed_norm<<<(unsigned)ceil_div(T, 4), 256, 0, s>>>(
-        T, D, R, V, eps, tokens, ro, reinterpret_cast<const uint16_t*>(emb), x, a, pos, offs);
+    const unsigned grid = (unsigned)ceil_div(T, 4);
+    const auto* eb = reinterpret_cast<const uint16_t*>(emb);
+    if (D <= 512)
+        k_embed_norm<1><<<grid, 256, 0, s>>>(T, D, R, V, eps, tokens, ro, eb, x, a, pos, offs);
+    else if (D <= 1024)
+        k_embed_norm<2><<<grid, 256, 0, s>>>(T, D, R, V, eps, tokens, ro, eb, x, a, pos, offs);
+    else if (D <= 2048)
+        k_embed_norm<4><<<grid, 256, 0, s>>>(T, D, R, V, eps, tokens, ro, eb, x, a, pos, offs);
+    else
+        k_embed_norm<0><<<grid, 256, 0, s>>>(T, D, R, V, eps, tokens, ro, eb, x, a, pos, offs);
     return hipGetLastError();
 }
 
