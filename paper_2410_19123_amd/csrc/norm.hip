@@ -17,18 +17,21 @@ __global__ __launch_bounds__(256) void k_rms_to_bf16(int64_t d, const float* __r
                                                      float eps, uint16_t* __restrict__ xn) {
     __shared__ float part[4];
     const int64_t j = blockIdx.x;
-    if (j >= offsets[E]) return;
     const float4* row = reinterpret_cast<const float4*>(x + j * d);
     const int n4 = (int)(d / 4);
     const int tid = threadIdx.x;
     float4 v[NV > 0 ? NV : 1];
     float ss = 0.0f;
     if constexpr (NV > 0) {
+        // The row (in bounds: the grid has one workgroup per row of x) is
+        // requested before the routed-row count, so the two round trips
+        // overlap.
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             const int c = tid + 256 * i;
             v[i] = c < n4 ? row[c] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
         }
+        if (j >= offsets[E]) return;
 #pragma unroll
         for (int i = 0; i < NV; ++i) {
             if (tid + 256 * i < n4) {
@@ -39,6 +42,7 @@ __global__ __launch_bounds__(256) void k_rms_to_bf16(int64_t d, const float* __r
             }
         }
     } else {
+        if (j >= offsets[E]) return;
         for (int c = tid; c < n4; c += 256) {
             const float4 w = row[c];
             ss += w.x * w.x;
