@@ -748,9 +748,10 @@ readme_status readme_rope(int64_t T, int32_t H, const int32_t *pos, void *x, int
  * about 2^-16 of the largest |v| plus the final bf16 rounding.
  *   q, k, v  [T][ld_in] bf16 (head h at columns 128h ..), o [T][ld_out] bf16
  *   out, pos [T] int32.  R, the number of requests the tokens form, only
- *   picks the launch shape (from a mean of 128 tokens per request, four
- *   waves per workgroup share each key block; below, one wave loops over
- *   its own queries' blocks): every R >= 0 gives the same bits.  Requires
+ *   picks the launch shape (from a mean of 128 tokens per request, eight
+ *   waves per 128 queries in two groups over alternate key blocks; below,
+ *   one wave per 32 queries over its own blocks); both meet the bound above,
+ *   their last bits may differ.  Requires
  *   ld_in, ld_out >= 128 H and multiples of 8, 16-byte aligned q, k, v, o,
  *   H <= 65535.  o must not overlap q, k or v.
  */

@@ -30,12 +30,12 @@ namespace {
 constexpr int kHeadDim = 128;
 // log2(e) / sqrt(128): scores go to exp2 in one multiply.
 constexpr float kScoreScale = 0.12751743082459868f;
-// Mean request length from which attention runs four waves per workgroup
-// sharing each key block (below it, one wave per workgroup loops only over
-// its own queries' blocks: a request batch of short requests then needs one
-// key block per wave and no wave waits at another's barrier).
+// Mean request length from which attention runs eight waves per workgroup
+// (128 queries, two wave groups over alternate key blocks, every block
+// shared by four waves); below it one wave per workgroup loops only over its
+// own queries' blocks (a request batch of short requests then needs one key
+// block per wave and no wave waits at another's barrier).
 constexpr int kAttnLongMean = 128;
-constexpr int kAttnLongWaves = 4;
 
 // First token of t's request, from the in-request position (clamped, so a
 // malformed position never leads outside [0, t]).
@@ -366,83 +366,99 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-// Causal attention of one 128-dim head over 32 * NW queries per workgroup.
-//   Wave w owns queries t = q0 + 32w + (lane % 32); both half-waves hold the
-//   same queries (the matrix-core layout splits each key block between
-//   them).  Per key block of 32 rows, staged in LDS (K row-major, V
-//   transposed):
+// Causal attention of one 128-dim head over 32 * QW queries per workgroup
+// (QW = NW / KS waves of queries, KS = 1 or 2 wave groups over the keys).
+//   Wave w owns queries t = q0 + 32 (w % QW) + (lane % 32); both half-waves
+//   hold the same queries (the matrix-core layout splits each 32-key block
+//   between them).  Per key block of 32 rows, staged in LDS (K row-major,
+//   V transposed):
 //     S^T = K Q^T     8 MFMAs 32x32x16, Q in registers, so each lane holds
 //                     16 of its query's 32 scores and the softmax needs one
 //                     cross-lane step (lane ^ 32);
 //     mask            key in [start(t), t] (same request, not after t);
-//     online softmax  running max m and sum l per query, fp32, exp2;
+//     online softmax  running max m and sum l per query, fp32, hardware
+//                     exp2 (a rescale by exactly 1 is skipped wave-wide);
 //     O^T += V^T P^T  P split into bf16 hi + lo parts (p - hi is exact in
-//                     fp32), 2 x 8 MFMAs, so the weights carry ~16 bits;
-//                     the key order of P's operand is the score layout's,
-//                     and V^T is read from LDS in the same order.
+//                     fp32) by the packed hardware conversion, 2 x 8 MFMAs,
+//                     so the weights carry ~16 bits; the key order of P's
+//                     operand is the score layout's, and V^T is read from
+//                     LDS in the same order.
 //   o = O / l, rounded to bf16.  Key blocks run from the first query's
 //   request start to the last query; a wave skips the blocks outside its own
 //   queries' range (the workgroup still passes every barrier).
 //   NW = 1 (short requests): each wave loads only its own blocks, one LDS
-//   buffer.  NW = 4 (long requests): the four waves share each block, two
-//   LDS buffers, and block kb+1 is requested into registers before block kb
+//   buffer.  NW = 8, KS = 2 (long requests): wave group g = w / 4 takes the
+//   blocks kb0 + 2i + g, so the longest chain of blocks is halved and each
+//   SIMD runs two waves; the eight waves load each pair of blocks together,
+//   two LDS buffers, the next pair requested into registers before this one
 //   is computed and written to the other buffer after it, one barrier per
-//   block.
-template <int NW>
+//   pair.  At the end group 1 hands (m, l, O) to group 0 through LDS, which
+//   merges the two online softmaxes: m = max(m0, m1), O = O0 2^(m0-m) +
+//   O1 2^(m1-m), l likewise.  The two forms add the keys in different
+//   orders, so their last bits may differ.
+template <int NW, int KS>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void k_attention_causal(int64_t T, const int32_t* __restrict__ pos,
                         const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
                         const uint16_t* __restrict__ v, int64_t ldi, uint16_t* __restrict__ o,
                         int64_t ldo) {
+    constexpr int QW = NW / KS;       // waves of distinct queries
     constexpr int KP = kHeadDim + 8;  // K rows in LDS, 272 bytes apart
     constexpr int VP = 32 + 8;        // V^T rows (one per dim), 80 bytes apart
-    constexpr bool PF = NW > 1;       // next block in flight during this one
+    constexpr bool PF = NW > 1;       // next blocks in flight during these
     constexpr int NB = PF ? 2 : 1;    // LDS buffers
-    constexpr int NCH = 32 * (kHeadDim / 8) / (64 * NW);  // 16-byte chunks per thread
-    __shared__ __attribute__((aligned(16))) uint16_t k_lds[NB][32 * KP];
-    __shared__ __attribute__((aligned(16))) uint16_t vt_lds[NB][kHeadDim * VP];
+    constexpr int NCH = KS * 32 * (kHeadDim / 8) / (64 * NW);  // 16-byte chunks per thread
+    static_assert(NCH >= 1 && KS * 32 * (kHeadDim / 8) == NCH * 64 * NW, "chunk split");
+    constexpr int BLK = 32 * KP + kHeadDim * VP;  // one key block (K, V^T), uint16
+    __shared__ __attribute__((aligned(16))) uint16_t lds[NB * KS * BLK];
+    auto k_at = [&](int b, int h) { return lds + (b * KS + h) * BLK; };
+    auto vt_at = [&](int b, int h) { return lds + (b * KS + h) * BLK + 32 * KP; };
 
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int qg = wv % QW, grp = wv / QW;
     const int hf = lane >> 5, col = lane & 31;
     const int64_t hoff = (int64_t)blockIdx.y * kHeadDim;
-    const int64_t q0 = (int64_t)blockIdx.x * (32 * NW);
-    const int64_t t = q0 + 32 * wv + col;
+    const int64_t q0 = (int64_t)blockIdx.x * (32 * QW);
+    const int64_t t = q0 + 32 * qg + col;
     const bool tv = t < T;
     const int64_t tq = tv ? t : T - 1;
     const int64_t start = request_start(tq, pos);
-    const int64_t wfirst = q0 + 32 * wv;
+    const int64_t wfirst = q0 + 32 * qg;
     const bool wact = wfirst < T;
     const int64_t wlo = request_start(wact ? wfirst : T - 1, pos);
     const int64_t whi = wfirst + 31 < T - 1 ? wfirst + 31 : T - 1;
     const int64_t lo = request_start(q0, pos);
-    const int64_t hi = q0 + 32 * NW - 1 < T - 1 ? q0 + 32 * NW - 1 : T - 1;
+    const int64_t hi = q0 + 32 * QW - 1 < T - 1 ? q0 + 32 * QW - 1 : T - 1;
+    const int64_t kb0 = lo >> 5, kb1 = hi >> 5;
 
-    // Chunk i of this thread: key row c / 16, 8 dims at 8 * (c % 16).
+    // Chunk i of this thread: block group c / 512, key row (c % 512) / 16 of
+    // that block, 8 dims at 8 * (c % 16).
     uint4 kr[NCH], vr[NCH];
-    auto fetch = [&](int64_t kb) {
+    auto fetch = [&](int64_t kbase) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             const int c = tid + i * 64 * NW;
-            const int64_t key = kb * 32 + (c >> 4);
+            const int64_t key = (kbase + (c >> 9)) * 32 + ((c & 511) >> 4);
             kr[i] = make_uint4(0u, 0u, 0u, 0u);
             vr[i] = kr[i];
-            if (key < T) {
+            if (key <= kb1 * 32 + 31 && key < T) {
                 kr[i] = *reinterpret_cast<const uint4*>(k + key * ldi + hoff + (c & 15) * 8);
                 vr[i] = *reinterpret_cast<const uint4*>(v + key * ldi + hoff + (c & 15) * 8);
             }
         }
     };
-    auto stash = [&](int b) {
+    auto stash = [&](int b) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < NCH; ++i) {
             const int c = tid + i * 64 * NW;
-            const int r = c >> 4, ch = c & 15;
-            *reinterpret_cast<uint4*>(&k_lds[b][r * KP + ch * 8]) = kr[i];
+            const int h = c >> 9, r = (c & 511) >> 4, ch = c & 15;
+            *reinterpret_cast<uint4*>(k_at(b, h) + r * KP + ch * 8) = kr[i];
+            uint16_t* vt = vt_at(b, h);
             const uint32_t vw[4] = {vr[i].x, vr[i].y, vr[i].z, vr[i].w};
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                vt_lds[b][(ch * 8 + 2 * e) * VP + r] = (uint16_t)(vw[e] & 0xffffu);
-                vt_lds[b][(ch * 8 + 2 * e + 1) * VP + r] = (uint16_t)(vw[e] >> 16);
+                vt[(ch * 8 + 2 * e) * VP + r] = (uint16_t)(vw[e] & 0xffffu);
+                vt[(ch * 8 + 2 * e + 1) * VP + r] = (uint16_t)(vw[e] >> 16);
             }
         }
     };
@@ -460,16 +476,17 @@ void k_attention_causal(int64_t T, const int32_t* __restrict__ pos,
         for (int r = 0; r < 16; ++r) acc[mt][r] = 0.0f;
     float m_run = -INFINITY, l_run = 0.0f;
 
-    auto compute = [&](int64_t kb, int b) {
+    auto compute = [&](int64_t kb, int b) __attribute__((always_inline)) {
         const int64_t k0 = kb * 32;
-        if (!(wact && k0 <= whi && k0 + 31 >= wlo)) return;
+        if (!(wact && kb <= kb1 && k0 <= whi && k0 + 31 >= wlo)) return;
+        const uint16_t* kl = k_at(b, grp);
+        const uint16_t* vl = vt_at(b, grp);
         f32x16 s;
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[r] = 0.0f;
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) {
-            const bf16x8 kf =
-                *reinterpret_cast<const bf16x8*>(&k_lds[b][col * KP + ks * 16 + hf * 8]);
+            const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kl + col * KP + ks * 16 + hf * 8);
             s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s, 0, 0, 0);
         }
         // lane holds keys k0 + 4*hf + off(r), off(r) = 8*(r/4) + (r%4), of
@@ -491,7 +508,7 @@ void k_attention_causal(int64_t T, const int32_t* __restrict__ pos,
         m_run = mn;
         l_run *= alpha;
         // The weights' hi and lo bf16 parts, two per instruction (the
-        // matrix-core conversion rounds to nearest even; p is finite)
+        // hardware conversion rounds to nearest even; p is finite)
         uint32_t ph[8], pl[8];
 #pragma unroll
         for (int r = 0; r < 16; r += 2) {
@@ -516,7 +533,7 @@ void k_attention_causal(int64_t T, const int32_t* __restrict__ pos,
             const u32x4 bl = {pl[4 * kk], pl[4 * kk + 1], pl[4 * kk + 2], pl[4 * kk + 3]};
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
-                const uint16_t* vp = &vt_lds[b][(mt * 32 + col) * VP + 16 * kk + 4 * hf];
+                const uint16_t* vp = vl + (mt * 32 + col) * VP + 16 * kk + 4 * hf;
                 const uint2 a0 = *reinterpret_cast<const uint2*>(vp);
                 const uint2 a1 = *reinterpret_cast<const uint2*>(vp + 8);
                 const u32x4 av = {a0.x, a0.y, a1.x, a1.y};
@@ -530,26 +547,55 @@ void k_attention_causal(int64_t T, const int32_t* __restrict__ pos,
         }
     };
 
-    const int64_t kb0 = lo >> 5, kb1 = hi >> 5;
+    // Steps of KS blocks: step p holds blocks kb0 + KS p .. + KS - 1.
+    const int64_t np = (kb1 - kb0 + KS) / KS;
     if constexpr (PF) {
         fetch(kb0);
-        stash((int)(kb0 & 1));
+        stash(0);
         __syncthreads();
-        for (int64_t kb = kb0; kb <= kb1; ++kb) {
-            const int b = (int)(kb & 1);
-            if (kb < kb1) fetch(kb + 1);
-            compute(kb, b);
-            if (kb < kb1) stash(b ^ 1);
+        for (int64_t p = 0; p < np; ++p) {
+            const int b = (int)(p & 1);
+            if (p + 1 < np) fetch(kb0 + KS * (p + 1));
+            compute(kb0 + KS * p + grp, b);
+            if (p + 1 < np) stash(b ^ 1);
             __syncthreads();
         }
     } else {
-        for (int64_t kb = kb0; kb <= kb1; ++kb) {
-            fetch(kb);
+        for (int64_t p = 0; p < np; ++p) {
+            fetch(kb0 + p);
             stash(0);
             __syncthreads();
-            compute(kb, 0);
+            compute(kb0 + p, 0);
             __syncthreads();
         }
+    }
+
+    if constexpr (KS == 2) {
+        // Group 1 hands its state to group 0 (the loop's last barrier has
+        // passed, so the LDS blocks are free): lane-major, 66 floats a lane.
+        float* xs = reinterpret_cast<float*>(lds) + qg * 66 * 64;
+        static_assert(QW * 66 * 64 * 4 <= NB * KS * BLK * 2, "merge area");
+        if (grp == 1) {
+            xs[lane] = m_run;
+            xs[64 + lane] = l_run;
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) xs[(2 + mt * 16 + r) * 64 + lane] = acc[mt][r];
+        }
+        __syncthreads();
+        if (grp == 1) return;
+        const float m1 = xs[lane], l1 = xs[64 + lane];
+        const float mn = fmaxf(m_run, m1);
+        const float base = mn == -INFINITY ? 0.0f : mn;
+        const float a0 = __builtin_amdgcn_exp2f(m_run - base);
+        const float a1 = __builtin_amdgcn_exp2f(m1 - base);
+        l_run = l_run * a0 + l1 * a1;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[mt][r] = acc[mt][r] * a0 + xs[(2 + mt * 16 + r) * 64 + lane] * a1;
     }
 
     const float lt = l_run + __shfl_xor(l_run, 32, 64);
@@ -643,12 +689,11 @@ hipError_t launch_attention(int64_t T, int H, int32_t R, const int32_t* pos, con
     const auto* vb = reinterpret_cast<const uint16_t*>(v);
     auto* ob = reinterpret_cast<uint16_t*>(o);
     if (T >= (int64_t)kAttnLongMean * (R > 0 ? R : 1)) {
-        const dim3 grid((unsigned)ceil_div(T, 32 * kAttnLongWaves), (unsigned)H);
-        k_attention_causal<kAttnLongWaves><<<grid, 64 * kAttnLongWaves, 0, s>>>(
-            T, pos, qb, kb, vb, ldi, ob, ldo);
+        const dim3 grid((unsigned)ceil_div(T, 128), (unsigned)H);
+        k_attention_causal<8, 2><<<grid, 512, 0, s>>>(T, pos, qb, kb, vb, ldi, ob, ldo);
     } else {
         const dim3 grid((unsigned)ceil_div(T, 32), (unsigned)H);
-        k_attention_causal<1><<<grid, 64, 0, s>>>(T, pos, qb, kb, vb, ldi, ob, ldo);
+        k_attention_causal<1, 1><<<grid, 64, 0, s>>>(T, pos, qb, kb, vb, ldi, ob, ldo);
     }
     return hipGetLastError();
 }

@@ -133,8 +133,9 @@ ATTN_CASES = [
 
 @pytest.mark.parametrize("lengths,H,scale", ATTN_CASES)
 def test_attention_matches_oracle(lengths, H, scale):
-    """Both launch shapes (one wave per workgroup, and four sharing each key
-    block with the next block in flight) on every case; the same bits."""
+    """Both launch shapes (one wave per 32 queries; eight waves per 128
+    queries in two groups over alternate key blocks, merged at the end) on
+    every case."""
     L = _lib()
     ro = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
     T = int(ro[-1])
@@ -146,7 +147,7 @@ def test_attention_matches_oracle(lengths, H, scale):
     short = from_dev(L.readme_attention_causal(dq, dk, dv, dp, H, R=max(T, 1)))
     long_ = from_dev(L.readme_attention_causal(dq, dk, dv, dp, H, R=1))
     _attention_ok(short, q, k, v, ro, f"attention {lengths} H={H}, one wave")
-    assert np.array_equal(short, long_), "launch shapes differ"
+    _attention_ok(long_, q, k, v, ro, f"attention {lengths} H={H}, split keys")
 
 
 def _forward(shape, lengths, seed, bad_tokens=False):
