@@ -369,8 +369,8 @@ TRAFFIC = {
                        "f2e5982ee17904e80e59c9f86a5a9dcabc2500a967656b365c81d094c306a252",
                        609159683, 23068672),
     "llama7b_decode32": (_STACK_SOURCES,
-                         "a756ab735425f3c3076cc6ab0098e362b9a17ea201cdde28fde69a3b168da6ea",
-                         7874059189, 56098816),
+                         "600e4d122b11f65a2481f6be9870ec15ad14c9dfec5c1e1f0542ef625b3bea90",
+                         7873977716, 56098816),
 }
 
 
