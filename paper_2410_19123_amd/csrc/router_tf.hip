@@ -16,7 +16,9 @@
 // The projections and the MLP run on the grouped-GEMM kernels with one
 // "expert" (offsets {0, T}).  Here: the embedding gather fused with the
 // first norm, the MLP's norm, RoPE, causal attention, and the final norm
-// fused with the gate (readme_route's canonical fp32 order).  Seven launches.
+// fused with the gate (readme_route's canonical fp32 order).  Nine launches
+// per call (embedding + norm, q|k|v, RoPE, attention, Wo, norm, gate/up, down,
+// norm + gate).
 #include <limits.h>
 #include <math.h>
 
