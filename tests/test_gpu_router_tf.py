@@ -277,6 +277,22 @@ def test_router_tf_shapes(oracle_mod, D, F, V, E, lengths):
     _end_to_end(w, tokens, ro, ids, logits)
 
 
+def test_router_tf_many_requests(oracle_mod):
+    """5000 requests (most of one token or empty) over 6000 tokens: the
+    request offsets no longer fit the workgroup's LDS copy, so positions come
+    from the search in global memory."""
+    L = _lib()
+    lengths = wl.ragged_lengths(6000, 5000, 7)
+    ro = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+    pos = from_dev(L.readme_request_positions(to_dev(ro), 6000))
+    assert np.array_equal(pos, R.positions(ro, 6000))
+    shape = wl.RouterShape(D=128, F=64, V=500, E=4)
+    w, tokens, ro2, ids, logits, g = _forward(shape, lengths, 7)
+    assert np.array_equal(ro2, ro)
+    _stage_checks(w, tokens, ro, ids, logits, g)
+    _end_to_end(w, tokens, ro, ids, logits)
+
+
 def test_router_tf_table1_request_batch(oracle_mod):
     """Table 1's router on the request batch (256 requests x 32 tokens), the
     launch the benchmark times; stages checked on eight sampled requests."""
