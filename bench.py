@@ -825,6 +825,7 @@ def main():
         out["decode"] = side_line("llama7b_decode32", args.side_steps, 3)
         out["prefill"] = side_line("prefill_skew16", args.side_steps, 3)
         out["router"] = router_line(args.side_steps, 3)
+        out["router_long"] = router_line(args.side_steps, 3, "prompts_8x1024")
     if args.library_gemm and w.dtype == "bf16" and w.layers == 1 and w.K == 1 and not w.P:
         out["library_gemm"] = library_gemm(w, counts)
     if not args.no_cpu_baseline:

@@ -18,7 +18,7 @@
 // first norm, the MLP's norm, RoPE, causal attention, and the final norm
 // fused with the gate (readme_route's canonical fp32 order).  Nine launches
 // per call (embedding + norm, q|k|v, RoPE, attention, Wo, norm, gate/up, down,
-// norm + gate).
+// norm + gate; the last is two, norm then gate, for D > 2048).
 #include <limits.h>
 #include <math.h>
 
