@@ -97,3 +97,21 @@ def test_traffic_entries_follow_their_sources(tmp_path, monkeypatch):
     for name in bench.TRAFFIC:
         assert bench.traffic_bytes(name) is None, name
     assert bench.traffic_bytes("tiny_f32") is None   # no entry
+
+
+def test_router_flops():
+    """The router's algorithmic work per call, from the shapes by hand: the
+    four D x D projections and the three MLP matrices (2 flops per weight
+    per token), the gate, and causal attention's two products (2 x 128
+    multiply-adds per (query, key) pair and head, each key up to the query
+    inside its request)."""
+    shape = wl.ROUTER_TABLE1          # D = F = 512, E = 8, four heads
+    per_token = 2 * (4 * 512 * 512 + 3 * 512 * 512 + 8 * 512)
+    # one request of 3 tokens: 1 + 2 + 3 = 6 (query, key) pairs
+    assert bench.router_flops(shape, [3]) == 3 * per_token + 6 * 4 * 128 * 4
+    # empty requests add nothing; pairs never cross requests
+    assert bench.router_flops(shape, [3, 0, 2]) == 5 * per_token + (6 + 3) * 4 * 128 * 4
+    # the request batch of the benchmark: 256 requests of 32 (528 pairs each)
+    f = bench.router_flops(shape, [32] * 256)
+    assert f == 8192 * per_token + 256 * 528 * 4 * 128 * 4
+    assert f / 1e9 == pytest.approx(30.41, abs=0.01)
