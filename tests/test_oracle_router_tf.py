@@ -152,3 +152,50 @@ def test_mlp_hidden_agrees_with_the_layer_oracle(oracle_mod):
                                want_xn=True)
     assert np.array_equal(xn, m)
     assert np.allclose(ours, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_router_with_zero_output_projections_is_the_gate_of_the_embedding(oracle_mod):
+    """Wo = 0 and W2 = 0: both residual branches add exact zeros, so the
+    block's output is the embedding itself and the logits are the gate of
+    its norm."""
+    rng = np.random.default_rng(8)
+    w = _weights(rng)
+    w["wo"] = np.zeros_like(w["wo"])
+    w["w2"] = np.zeros_like(w["w2"])
+    tokens = rng.integers(0, 50, 9)
+    out = _run(w, tokens, np.array([0, 4, 9]))
+    x0 = R.embed(tokens, w["emb"])
+    assert np.array_equal(out["x1"], x0) and np.array_equal(out["x2"], x0)
+    ids, logits = oracle_mod.route(R.rmsnorm_bf16(x0), w["w_router"], w["bias"])
+    assert np.array_equal(out["ids"], ids) and np.array_equal(out["logits"], logits)
+
+
+def test_router_with_zero_queries_averages_the_prefix(oracle_mod):
+    """Wq = 0: every score is 0, so each token's attention output is the
+    plain mean of its request's value rows up to itself."""
+    rng = np.random.default_rng(9)
+    w = _weights(rng)
+    w["wq"] = np.zeros_like(w["wq"])
+    tokens = rng.integers(0, 50, 11)
+    ro = np.array([0, 5, 5, 11])
+    out = _run(w, tokens, ro)
+    v = R._f(out["v"])
+    mean = np.empty_like(v)
+    for r in range(len(ro) - 1):
+        a, b = ro[r], ro[r + 1]
+        mean[a:b] = np.cumsum(v[a:b], axis=0) / np.arange(1, b - a + 1)[:, None]
+    assert np.allclose(R._f(out["o"]), mean, rtol=2.0 ** -8, atol=1e-30)
+
+
+def test_router_mlp_reads_the_attention_residual(oracle_mod):
+    """The MLP branch is the layer oracle applied to x1 (the residual after
+    attention), not to the embedding."""
+    rng = np.random.default_rng(10)
+    w = _weights(rng)
+    tokens = rng.integers(0, 50, 7)
+    out = _run(w, tokens, np.array([0, 7]))
+    x1 = out["x1"]
+    assert not np.array_equal(x1, R.embed(tokens, w["emb"]))
+    delta = oracle_mod.layer(x1, np.array([0, 7], np.int32), w["w1"][None], w["w3"][None],
+                             w["w2"][None])
+    assert np.array_equal(out["x2"], (x1.astype(np.float64) + delta).astype(np.float32))
