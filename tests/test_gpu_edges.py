@@ -1,6 +1,7 @@
 """Edge cases of the HIP path against the CPU oracle: top-K with every expert
 selected (K = E), top-K selection among the largest expert count with
-heavy ties and NaN logits, and stacks with no layers or no tokens."""
+heavy ties and NaN logits, stacks with no layers or no tokens, and a
+131072-token layer over 64 experts."""
 import numpy as np
 import pytest
 import torch
@@ -80,3 +81,34 @@ def test_stack_without_layers_or_tokens(L):
     L.readme_moe_ffn_stack(empty, U.to_dev(np.zeros(w.E + 1, np.int32)), [packed], w.E, w.I)
     torch.cuda.synchronize()
     assert (U.from_dev(x) == before).all()
+
+
+def test_large_batch_fused_layer(L, oracle_mod):
+    """131072 tokens over 64 experts (d = 512, I = 320, Zipf-skewed ids): the
+    many-workgroup grouping bit-exact, and the fused FFN's largest grids
+    (thousands of workgroups per class of the mixed launch) on 4096 sampled
+    rows spread over every expert."""
+    T, d, E, I = 131072, 512, 64, 320
+    _say("large batch", T, E)
+    w = wl.Workload("large", T=T, d=d, E=E, I=I, dtype="bf16")
+    x = wl.make_x(w, 11)
+    rng = np.random.default_rng(11)
+    p = 1.0 / np.arange(1, E + 1)
+    ids = rng.choice(E, size=T, p=p / p.sum()).astype(np.int32)
+    wg, wu, wd = wl.make_experts(w, 11)
+    xd = U.to_dev(x)
+    counts, offs, perm, inv, _ = L.readme_group_by_expert(U.to_dev(ids), E)
+    packed = L.readme_pack_experts(*U.weights_to_dev(wg, wu, wd))
+    y = L.readme_moe_ffn_fused(xd, perm, offs, packed, E, I)
+    torch.cuda.synchronize()
+    c_ref, o_ref, p_ref, i_ref = oracle_mod.group(ids, E)
+    assert (U.from_dev(counts) == c_ref).all() and (U.from_dev(offs) == o_ref).all()
+    assert (U.from_dev(perm) == p_ref).all() and (U.from_dev(inv) == i_ref).all()
+    # 64 grouped rows from each expert's block (or all of a small block)
+    rows = np.concatenate([np.linspace(o_ref[e], o_ref[e + 1] - 1, 64).astype(np.int64)
+                           for e in range(E) if o_ref[e + 1] > o_ref[e]])
+    rows = np.unique(rows)
+    x_g = oracle_mod.gather(x, p_ref)
+    ref = oracle_mod.moe_ffn(x_g, o_ref, wg, wu, wd, rows=rows)
+    got = U.from_dev(y)[p_ref[rows]]
+    U.close(got, ref, "large batch")
