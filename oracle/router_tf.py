@@ -4,8 +4,8 @@ reads the current and all previous tokens of the sequence; Table 1: one
 layer, four heads, embedding, feature and MLP width 512, SwiGLU, RoPE,
 RMSNorm; Eq. 2: G's output picks the expert).
 
-TEST INFRASTRUCTURE.  Only the test suite and the CPU-baseline leg of the
-benchmark use this module; the product path never does.
+TEST INFRASTRUCTURE.  Only the test suite and the smoke check use this
+module; the product path never does.
 
 Reading (the paper gives the block's type and sizes, not its wiring):
   x0 = E[token]                       fp32 residual (bf16 table entries)
